@@ -1,0 +1,49 @@
+"""Plain, slow float64 CPU oracle of the Prefilling-dLLM block-sparse attention path.
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path may import, call or run
+anything in this package: only the test suite, ``__graft_entry__.smoke()`` and
+the ``cpu_baseline`` leg of ``bench.py`` use it.  It shares no code with the
+HIP library (no kernels, headers, helpers or generated tables) and imports
+nothing from it.
+
+Every function works on numpy arrays holding the exact values the GPU path
+receives (bf16 or fp32 inputs upcast exactly to float64) and computes in
+float64 with materialised score matrices and an explicit two-pass softmax, so
+that each step can be checked against the paper by eye:
+
+* ``prefill``  -- stage (a): chunk prefill (Section 5.1, Eq. 2), the chunk
+  cache, the chunk key summary and the intra-chunk eviction score (Section 5.2,
+  Eq. 5).
+* ``select``   -- stage (b): chunk scores, top-K chunks and top-B tokens per
+  kept chunk (Section 5.2, inter- and intra-chunk sparsity).
+* ``decode``   -- stage (c): attention of the decode block over the selected
+  prefix KV, the static query KV and its own KV (Section 5.3, prefix reuse).
+
+Parity status of each function is stated in its docstring ("pinned by ...").
+"""
+
+from .prefill import (
+    chunk_rows,
+    chunk_probs,
+    prefill_unit_ref,
+    prefill_ref,
+    cache_ref,
+    key_mean_ref,
+)
+from .select import chunk_scores_ref, topk_ref, score_select_ref
+from .decode import decode_kv_rows, decode_unit_ref, decode_ref
+
+__all__ = [
+    "chunk_rows",
+    "chunk_probs",
+    "prefill_unit_ref",
+    "prefill_ref",
+    "cache_ref",
+    "key_mean_ref",
+    "chunk_scores_ref",
+    "topk_ref",
+    "score_select_ref",
+    "decode_kv_rows",
+    "decode_unit_ref",
+    "decode_ref",
+]

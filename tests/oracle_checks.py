@@ -1,0 +1,329 @@
+"""Pins for the oracle: each check compares it with something other than itself.
+
+Every check reaches the oracle through its submodules at call time
+(``oracle.prefill.prefill_ref`` ...), so the mutation tests can plant a
+mistake in one oracle step with ``monkeypatch`` and confirm that some check
+fails.  Pins used:
+
+* hand-derived worked examples (``tests/golden/*.json``; the paper prints no
+  numeric example, so each fixture derives its values from the definitions);
+* brute force: the N chunk sequences concatenated with an explicit
+  block-diagonal -inf mask and a dense softmax (scipy); subset enumeration for
+  top-K;
+* library routines: torch scaled_dot_product_attention in float64 on the CPU,
+  numpy stable argsort;
+* closed forms: Q = 0, V = constant, constant content keys;
+* invariants: probability rows sum to one, KV-row permutation invariance.
+"""
+
+import itertools
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import scipy.special
+import torch
+
+import oracle.decode as OD
+import oracle.prefill as OP
+import oracle.select as OS
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _frac(x):
+    return float(Fraction(x))
+
+
+def _load(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def tiny_prefill_inputs(seed, B=2, N=3, C=5, Lq=2, Lm=3, Hq=4, Hkv=2, d=8, per_chunk=False):
+    rng = np.random.default_rng(seed)
+    qm_shape = (B, N, Lq + Lm) if per_chunk else (B, Lq + Lm)
+    return {
+        "q_pre": rng.standard_normal((B, N, 1 + C, Hq, d)),
+        "k_pre": rng.standard_normal((B, N, 1 + C, Hkv, d)),
+        "v_pre": rng.standard_normal((B, N, 1 + C, Hkv, d)),
+        "q_qm": rng.standard_normal(qm_shape + (Hq, d)),
+        "k_qm": rng.standard_normal(qm_shape + (Hkv, d)),
+        "v_qm": rng.standard_normal(qm_shape + (Hkv, d)),
+    }
+
+
+def _prefill(x, Lq, scale=None):
+    return OP.prefill_ref(x["q_pre"], x["k_pre"], x["v_pre"], x["q_qm"], x["k_qm"], x["v_qm"], Lq, scale)
+
+
+# ----------------------------------------------------------------------------- stage (a)
+
+def check_prefill_golden():
+    g = _load("prefill_worked_example.json")
+    x = {k: np.array(g[k], dtype=np.float64) for k in ("q_pre", "k_pre", "v_pre", "q_qm", "k_qm", "v_qm")}
+    r = _prefill(x, g["dims"]["L_q"], g["dims"]["scale"])
+    want_o = np.array([[_frac(v) for v in row] for row in g["expect_o_rows"]])
+    np.testing.assert_allclose(r["o"][0, 0, :, 0, :], want_o, rtol=0, atol=1e-12)
+    want_e = np.array([_frac(v) for v in g["expect_tok_score"]])
+    np.testing.assert_allclose(r["tok_score"][0, 0], want_e, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(r["lse"][0, 0, 0], np.log(np.array(g["expect_lse_of"], float)), atol=1e-12)
+    np.testing.assert_allclose(r["key_mean"][0, 0, 0], g["expect_key_mean"], atol=1e-15)
+    u = OP.prefill_unit_ref(x["q_pre"], x["k_pre"], x["v_pre"], x["q_qm"], x["k_qm"], x["v_qm"],
+                            0, 0, 0, g["dims"]["L_q"], g["dims"]["scale"])
+    want_p = np.array([[_frac(v) for v in row] for row in g["expect_probs"]])
+    np.testing.assert_allclose(u["p"], want_p, rtol=0, atol=1e-12)
+
+
+def check_prefill_blockdiag_bruteforce(seed, per_chunk=False):
+    """Concatenate the N chunk sequences of each (b, h), mask across chunks with -inf,
+    take one dense softmax and compare O, LSE and the Eq. 5 score (explicit loops)."""
+    B, N, C, Lq, Lm, Hq, Hkv, d = 2, 3, 5, 2, 3, 4, 2, 8
+    x = tiny_prefill_inputs(seed, B, N, C, Lq, Lm, Hq, Hkv, d, per_chunk)
+    scale = 1.0 / np.sqrt(d)
+    r = _prefill(x, Lq)
+    sc = 1 + C + Lq + Lm
+    tot = N * sc
+    for b in range(B):
+        e_bf = np.zeros((N, C))
+        for h in range(Hq):
+            g = h // (Hq // Hkv)
+            Q = np.zeros((tot, d))
+            K = np.zeros((tot, d))
+            V = np.zeros((tot, d))
+            owner = np.zeros(tot, dtype=int)
+            for n in range(N):
+                for s in range(sc):
+                    row = n * sc + s
+                    owner[row] = n
+                    if s <= C:
+                        Q[row], K[row], V[row] = x["q_pre"][b, n, s, h], x["k_pre"][b, n, s, g], x["v_pre"][b, n, s, g]
+                    else:
+                        j = s - 1 - C
+                        src = (lambda t: t[b, n, j]) if per_chunk else (lambda t: t[b, j])
+                        Q[row], K[row], V[row] = src(x["q_qm"])[h], src(x["k_qm"])[g], src(x["v_qm"])[g]
+            mask = np.where(owner[:, None] == owner[None, :], 0.0, -np.inf)
+            S = scale * Q @ K.T + mask
+            P = scipy.special.softmax(S, axis=1)
+            O = P @ V
+            lse = scipy.special.logsumexp(S, axis=1)
+            for n in range(N):
+                rows = slice(n * sc, (n + 1) * sc)
+                np.testing.assert_allclose(r["o"][b, n, :, h, :], O[rows], rtol=0, atol=1e-12)
+                np.testing.assert_allclose(r["lse"][b, n, h], lse[rows], rtol=0, atol=1e-12)
+                for j in range(C):
+                    cj = n * sc + 1 + j
+                    for k in range(Lq):
+                        qk = n * sc + 1 + C + k
+                        e_bf[n, j] += P[qk, cj] + P[cj, qk]
+        np.testing.assert_allclose(r["tok_score"][b], e_bf, rtol=0, atol=1e-12)
+
+
+def check_prefill_sdpa(seed):
+    """Per-chunk O against torch's scaled_dot_product_attention (float64, CPU)."""
+    B, N, C, Lq, Lm, Hq, Hkv, d = 1, 2, 9, 3, 4, 6, 2, 16
+    x = tiny_prefill_inputs(seed, B, N, C, Lq, Lm, Hq, Hkv, d)
+    r = _prefill(x, Lq)
+    for b in range(B):
+        for n in range(N):
+            q = np.concatenate([x["q_pre"][b, n], x["q_qm"][b]], axis=0)       # (Sc, Hq, d)
+            k = np.concatenate([x["k_pre"][b, n], x["k_qm"][b]], axis=0)
+            v = np.concatenate([x["v_pre"][b, n], x["v_qm"][b]], axis=0)
+            rep = Hq // Hkv
+            qt = torch.from_numpy(q).permute(1, 0, 2)
+            kt = torch.from_numpy(np.repeat(k, rep, axis=1)).permute(1, 0, 2)
+            vt = torch.from_numpy(np.repeat(v, rep, axis=1)).permute(1, 0, 2)
+            ot = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt).permute(1, 0, 2).numpy()
+            np.testing.assert_allclose(r["o"][b, n], ot, rtol=0, atol=1e-12)
+
+
+def check_prefill_q_zero(seed):
+    """Q = 0: every probability is 1/S_c, O is the mean of the V rows, e_j = 2 Hq Lq / S_c."""
+    B, N, C, Lq, Lm, Hq, Hkv, d = 1, 2, 6, 3, 2, 4, 1, 8
+    x = tiny_prefill_inputs(seed, B, N, C, Lq, Lm, Hq, Hkv, d)
+    x["q_pre"][:] = 0
+    x["q_qm"][:] = 0
+    r = _prefill(x, Lq)
+    sc = 1 + C + Lq + Lm
+    for n in range(N):
+        vrows = np.concatenate([x["v_pre"][0, n, :, 0], x["v_qm"][0, :, 0]], axis=0)
+        for h in range(Hq):
+            np.testing.assert_allclose(r["o"][0, n, :, h], np.broadcast_to(vrows.mean(axis=0), (sc, d)), atol=1e-12)
+        np.testing.assert_allclose(r["lse"][0, n], np.log(sc), atol=1e-12)
+    np.testing.assert_allclose(r["tok_score"], 2.0 * Hq * Lq / sc, atol=1e-12)
+
+
+def check_prefill_v_const(seed):
+    """V rows all equal to one vector v: O = v in every row and head."""
+    x = tiny_prefill_inputs(seed)
+    v = np.arange(x["v_pre"].shape[-1], dtype=np.float64) - 3.5
+    x["v_pre"][:] = v
+    x["v_qm"][:] = v
+    r = _prefill(x, 2)
+    np.testing.assert_allclose(r["o"], np.broadcast_to(v, r["o"].shape), atol=1e-12)
+
+
+def check_prefill_rowsums(seed):
+    """Every probability row is non-negative and sums to one."""
+    x = tiny_prefill_inputs(seed)
+    for (b, n, h) in [(0, 0, 0), (1, 2, 3), (0, 1, 2)]:
+        u = OP.prefill_unit_ref(x["q_pre"], x["k_pre"], x["v_pre"], x["q_qm"], x["k_qm"], x["v_qm"], b, n, h, 2)
+        assert (u["p"] >= 0).all()
+        np.testing.assert_allclose(u["p"].sum(axis=1), 1.0, atol=1e-12)
+
+
+def check_cache_exact(seed):
+    """The cache is the chunk's BOS + content rows, bit for bit, at [b][n][g][slot]."""
+    x = tiny_prefill_inputs(seed)
+    kp = x["k_pre"].astype(np.float32)
+    kc = OP.cache_ref(kp)
+    assert kc.dtype == np.float32
+    B, N, C1, Hkv, d = kp.shape
+    for b, n, g, s in itertools.product(range(B), range(N), range(Hkv), range(C1)):
+        assert np.array_equal(kc[b, n, g, s], kp[b, n, s, g])
+
+
+def check_key_mean_const(seed):
+    """Content keys equal to one vector per (b, n, g) and a random BOS row: the mean is that vector."""
+    x = tiny_prefill_inputs(seed)
+    k = x["k_pre"].copy()
+    B, N, C1, Hkv, d = k.shape
+    const = np.random.default_rng(seed + 1).standard_normal((B, N, Hkv, d))
+    k[:, :, 1:] = const[:, :, None]
+    np.testing.assert_allclose(OP.key_mean_ref(k), const, atol=1e-14)
+
+
+# ----------------------------------------------------------------------------- stage (b)
+
+def check_select_golden():
+    g = _load("select_worked_example.json")
+    q = np.array(g["q_dec"], float)
+    km = np.array(g["key_mean"], float)
+    ts = np.array(g["tok_score"], float)
+    s = OS.chunk_scores_ref(q, km, g["dims"]["scale"])
+    np.testing.assert_allclose(s[0], g["expect_scores"], atol=1e-12)
+    for case in g["cases"]:
+        ci, tsl, _ = OS.score_select_ref(q, km, ts, case["top_k"], case["tok_budget"], g["dims"]["scale"])
+        assert ci[0].tolist() == case["chunk_idx"], case
+        assert tsl[0].tolist() == case["tok_slot"], case
+
+
+def check_chunk_score_zero_query(seed):
+    """Q_dec = 0: all scores 0, so the first K chunks are kept (ties to the lower index)."""
+    rng = np.random.default_rng(seed)
+    q = np.zeros((2, 5, 4, 8))
+    km = rng.standard_normal((2, 7, 2, 8))
+    e = rng.standard_normal((2, 7, 6))
+    ci, _, s = OS.score_select_ref(q, km, e, 3, 2)
+    assert np.all(s == 0)
+    assert ci.tolist() == [[0, 1, 2], [0, 1, 2]]
+
+
+def check_chunk_score_linear(seed):
+    """The score is linear in the decode queries: 2 Q_dec -> 2 s; Q1 + Q2 -> s1 + s2."""
+    rng = np.random.default_rng(seed)
+    q1, q2 = rng.standard_normal((2, 1, 6, 4, 8))
+    km = rng.standard_normal((1, 5, 2, 8))
+    s1 = OS.chunk_scores_ref(q1, km)
+    s2 = OS.chunk_scores_ref(q2, km)
+    np.testing.assert_allclose(OS.chunk_scores_ref(2 * q1, km), 2 * s1, atol=1e-12)
+    np.testing.assert_allclose(OS.chunk_scores_ref(q1 + q2, km), s1 + s2, atol=1e-12)
+
+
+def check_chunk_score_gqa_groups(seed):
+    """Query head h reads KV head h // (Hq/Hkv): queries only in heads 2, 3 (group 1) and key
+    means only in KV head 0 give all-zero scores; key means in KV head 1 give non-zero ones."""
+    rng = np.random.default_rng(seed)
+    q = np.zeros((1, 3, 4, 8))
+    q[:, :, 2:] = rng.standard_normal((1, 3, 2, 8))
+    km = np.zeros((1, 4, 2, 8))
+    km[:, :, 0] = rng.standard_normal((1, 4, 8))
+    assert np.all(OS.chunk_scores_ref(q, km) == 0)
+    km2 = np.zeros((1, 4, 2, 8))
+    km2[:, :, 1] = rng.standard_normal((1, 4, 8))
+    assert np.all(OS.chunk_scores_ref(q, km2) != 0)
+
+
+def check_topk_bruteforce(seed):
+    """Among all size-k subsets exactly one has every member ranking above every
+    non-member (score descending, index ascending); it is the oracle's answer."""
+    rng = np.random.default_rng(seed)
+    for trial in range(30):
+        n = int(rng.integers(1, 8))
+        x = rng.integers(-3, 4, size=n).astype(np.float64)      # many ties
+        for k in range(1, n + 1):
+            def beats(i, j):
+                return x[i] > x[j] or (x[i] == x[j] and i < j)
+            good = [set(c) for c in itertools.combinations(range(n), k)
+                    if all(beats(i, j) for i in c for j in range(n) if j not in c)]
+            assert len(good) == 1
+            got = OS.topk_ref(x, k)
+            assert set(got.tolist()) == good[0]
+            assert list(got) == sorted(got)
+            stable = np.sort(np.argsort(-x, kind="stable")[:k])
+            assert np.array_equal(got, stable)
+
+
+# ----------------------------------------------------------------------------- stage (c)
+
+def check_decode_golden():
+    g = _load("decode_worked_example.json")
+    a = {k: np.array(g[k], float) for k in ("q_dec", "k_dec", "v_dec", "k_cache", "v_cache", "k_static", "v_static")}
+    ci = np.array(g["chunk_idx"], np.int32)
+    ts = np.array(g["tok_slot"], np.int32)
+    o, lse = OD.decode_ref(a["q_dec"], a["k_dec"], a["v_dec"], a["k_cache"], a["v_cache"], ci, ts,
+                           a["k_static"], a["v_static"], g["dims"]["n_static"], g["dims"]["scale"])
+    np.testing.assert_allclose(o[0, 0, 0], [_frac(v) for v in g["expect_o"]], atol=1e-12)
+    np.testing.assert_allclose(lse[0, 0, 0], np.log(g["expect_lse_of"]), atol=1e-12)
+
+
+def tiny_decode_inputs(seed, B=2, N=4, C=6, Ld=3, Ls=4, Hq=4, Hkv=2, d=8):
+    rng = np.random.default_rng(seed)
+    return {
+        "q_dec": rng.standard_normal((B, Ld, Hq, d)),
+        "k_dec": rng.standard_normal((B, Ld, Hkv, d)),
+        "v_dec": rng.standard_normal((B, Ld, Hkv, d)),
+        "k_cache": rng.standard_normal((B, N, Hkv, 1 + C, d)),
+        "v_cache": rng.standard_normal((B, N, Hkv, 1 + C, d)),
+        "k_static": rng.standard_normal((B, Ls, Hkv, d)),
+        "v_static": rng.standard_normal((B, Ls, Hkv, d)),
+    }
+
+
+def _decode(x, ci, ts, n_static):
+    return OD.decode_ref(x["q_dec"], x["k_dec"], x["v_dec"], x["k_cache"], x["v_cache"], ci, ts,
+                         x["k_static"], x["v_static"], n_static)
+
+
+def check_decode_dense(seed, n_static=4):
+    """K = N and every slot kept: dense attention over all N(1+C) cache rows, the static
+    rows and the decode rows (torch SDPA and logsumexp, float64)."""
+    B, N, C, Ld, Ls, Hq, Hkv, d = 2, 4, 6, 3, 4, 4, 2, 8
+    x = tiny_decode_inputs(seed, B, N, C, Ld, Ls, Hq, Hkv, d)
+    ci = np.tile(np.arange(N, dtype=np.int32), (B, 1))
+    ts = np.tile(np.arange(1, C + 1, dtype=np.int32), (B, N, 1))
+    o, lse = _decode(x, ci, ts, n_static)
+    scale = 1.0 / np.sqrt(d)
+    for b in range(B):
+        for h in range(Hq):
+            g = h // (Hq // Hkv)
+            k = np.concatenate([x["k_cache"][b, :, g].reshape(-1, d), x["k_static"][b, :n_static, g], x["k_dec"][b, :, g]])
+            v = np.concatenate([x["v_cache"][b, :, g].reshape(-1, d), x["v_static"][b, :n_static, g], x["v_dec"][b, :, g]])
+            q = torch.from_numpy(x["q_dec"][b, :, h])
+            ot = torch.nn.functional.scaled_dot_product_attention(q[None], torch.from_numpy(k)[None], torch.from_numpy(v)[None])[0]
+            np.testing.assert_allclose(o[b, :, h], ot.numpy(), atol=1e-12)
+            lt = torch.logsumexp(scale * q @ torch.from_numpy(k).T, dim=1).numpy()
+            np.testing.assert_allclose(lse[b, h], lt, atol=1e-12)
+
+
+def check_decode_permutation(seed):
+    """Listing the kept chunks and slots in another order leaves O unchanged."""
+    x = tiny_decode_inputs(seed)
+    rng = np.random.default_rng(seed)
+    ci = np.array([[0, 2], [1, 3]], np.int32)
+    ts = np.sort(rng.permuted(np.tile(np.arange(1, 7), (2, 2, 1)), axis=2)[:, :, :3], axis=2).astype(np.int32)
+    o1, l1 = _decode(x, ci, ts, 2)
+    o2, l2 = _decode(x, ci[:, ::-1].copy(), ts[:, ::-1, ::-1].copy(), 2)
+    np.testing.assert_allclose(o1, o2, atol=1e-12)
+    np.testing.assert_allclose(l1, l2, atol=1e-12)

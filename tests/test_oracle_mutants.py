@@ -1,0 +1,131 @@
+"""Plant plausible mistakes in the oracle (on the CPU) and check that a pin fails.
+
+Each mutant replaces one oracle step through ``monkeypatch``; the test passes
+only if every pin listed for it raises.
+"""
+
+import numpy as np
+import pytest
+
+import oracle.decode as OD
+import oracle.prefill as OP
+import oracle.select as OS
+import oracle_checks as C
+
+
+def _softmax_cols(q_rows, k_rows, scale):
+    s = scale * (q_rows @ k_rows.T)
+    m = s.max(axis=0, keepdims=True)
+    ex = np.exp(s - m)
+    z = ex.sum(axis=0, keepdims=True)
+    return ex / z, (m + np.log(z))[0]
+
+
+def _probs_no_scale(q_rows, k_rows, scale):
+    return _orig_probs(q_rows, k_rows, 1.0)
+
+
+_orig_probs = OP.chunk_probs
+_orig_unit = OP.prefill_unit_ref
+
+
+def _unit_one_sided(*a, **k):
+    u = _orig_unit(*a, **k)
+    p = u["p"]
+    c1 = a[0].shape[2]
+    q_len = a[9]
+    u["e_head"] = p[c1:c1 + q_len, 1:c1].sum(axis=0)
+    return u
+
+
+def _unit_twice_first(*a, **k):
+    u = _orig_unit(*a, **k)
+    p = u["p"]
+    c1 = a[0].shape[2]
+    q_len = a[9]
+    u["e_head"] = 2 * p[c1:c1 + q_len, 1:c1].sum(axis=0)
+    return u
+
+
+def _unit_includes_m_rows(*a, **k):
+    u = _orig_unit(*a, **k)
+    p = u["p"]
+    c1 = a[0].shape[2]
+    u["e_head"] = p[c1:, 1:c1].sum(axis=0) + p[1:c1, c1:].sum(axis=1)
+    return u
+
+
+def _key_mean_with_bos(k_pre):
+    return np.asarray(k_pre, np.float64).mean(axis=2)
+
+
+def _topk_high_index(x, k):
+    x = np.asarray(x, np.float64)
+    order = np.lexsort((-np.arange(x.shape[0]), -x))
+    return np.sort(order[:k])
+
+
+def _scores_wrong_group(q_dec, key_mean, scale=None):
+    q = np.asarray(q_dec, np.float64)
+    km = np.asarray(key_mean, np.float64)
+    hkv = km.shape[2]
+    d = q.shape[3]
+    scale = 1 / np.sqrt(d) if not scale else scale
+    qbar = q.mean(axis=1)
+    s = np.zeros((q.shape[0], km.shape[1]))
+    for h in range(q.shape[2]):
+        s += scale * np.einsum("bd,bnd->bn", qbar[:, h], km[:, :, h % hkv])
+    return s
+
+
+_orig_rows = OD.decode_kv_rows
+
+
+def _rows_no_bos(x_cache, x_static, x_dec, chunk_idx, tok_slot, n_static, b, g):
+    parts = [np.asarray(x_cache[b, n, g, np.asarray(tok_slot)[b, kk]], np.float64)
+             for kk, n in enumerate(np.asarray(chunk_idx)[b])]
+    parts.append(np.asarray(x_static[b, :n_static, g], np.float64))
+    parts.append(np.asarray(x_dec[b, :, g], np.float64))
+    return np.concatenate(parts)
+
+
+def _rows_no_static(x_cache, x_static, x_dec, chunk_idx, tok_slot, n_static, b, g):
+    return _orig_rows(x_cache, x_static, x_dec, chunk_idx, tok_slot, 0, b, g)
+
+
+def _rows_slot_off_by_one(x_cache, x_static, x_dec, chunk_idx, tok_slot, n_static, b, g):
+    return _orig_rows(x_cache, x_static, x_dec, chunk_idx, np.asarray(tok_slot) - 1, n_static, b, g)
+
+
+MUTANTS = [
+    ("softmax over columns", OP, "chunk_probs", _softmax_cols,
+     [C.check_prefill_golden, lambda: C.check_prefill_sdpa(3)]),
+    ("scale dropped", OP, "chunk_probs", _probs_no_scale,
+     [lambda: C.check_prefill_sdpa(3), lambda: C.check_prefill_blockdiag_bruteforce(1)]),
+    ("Eq. 5 one-sided", OP, "prefill_unit_ref", _unit_one_sided,
+     [C.check_prefill_golden, lambda: C.check_prefill_q_zero(5)]),
+    ("Eq. 5 second term transposed", OP, "prefill_unit_ref", _unit_twice_first,
+     [C.check_prefill_golden, lambda: C.check_prefill_blockdiag_bruteforce(1)]),
+    ("Eq. 5 counts the pseudo-label rows", OP, "prefill_unit_ref", _unit_includes_m_rows,
+     [C.check_prefill_golden, lambda: C.check_prefill_q_zero(5)]),
+    ("key mean includes BOS", OP, "key_mean_ref", _key_mean_with_bos,
+     [C.check_prefill_golden, lambda: C.check_key_mean_const(9)]),
+    ("ties to the higher index", OS, "topk_ref", _topk_high_index,
+     [C.check_select_golden, lambda: C.check_topk_bruteforce(13)]),
+    ("query head mapped to the wrong KV head", OS, "chunk_scores_ref", _scores_wrong_group,
+     [lambda: C.check_chunk_score_gqa_groups(12)]),
+    ("decode drops the chunk BOS rows", OD, "decode_kv_rows", _rows_no_bos,
+     [C.check_decode_golden, lambda: C.check_decode_dense(14)]),
+    ("decode drops the static rows", OD, "decode_kv_rows", _rows_no_static,
+     [C.check_decode_golden, lambda: C.check_decode_dense(14)]),
+    ("decode slot off by one", OD, "decode_kv_rows", _rows_slot_off_by_one,
+     [C.check_decode_golden]),
+]
+
+
+@pytest.mark.parametrize("name,mod,attr,repl,checks", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(monkeypatch, name, mod, attr, repl, checks):
+    monkeypatch.setattr(mod, attr, repl)
+    for chk in checks:
+        with pytest.raises(Exception):
+            chk()
