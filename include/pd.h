@@ -1,0 +1,179 @@
+/*
+ * pd.h -- C ABI of the MI355X (gfx950) block-sparse attention path of
+ * Prefilling-dLLM: chunked prefill, per-step chunk/token selection, and
+ * sparse decode attention.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Plain C.  No HIP or torch types: device buffers are `void *` (or typed
+ *   pointers to device memory), the stream is a `hipStream_t` passed as
+ *   `void *` (NULL = the default stream).
+ * - Ownership: every pointer is caller-owned DEVICE memory, contiguous in the
+ *   layout stated next to it, 16-byte aligned.  The library allocates nothing,
+ *   frees nothing and never synchronises; every call only enqueues kernels on
+ *   `stream` and returns.  Scratch space is the caller's `workspace`, sized by
+ *   pd_workspace_bytes().  Calls on different streams must not share outputs
+ *   or workspace.
+ * - Errors: arguments are checked on the host before anything is launched; on
+ *   error nothing is launched, no output is touched, a status is returned and
+ *   a thread-local message is kept for pd_last_error_message().  A failed
+ *   launch returns PD_ERR_HIP.  Faults inside a kernel surface at the caller's
+ *   next synchronisation on `stream`.
+ * - Element type: all Q/K/V/O/cache tensors of one call have the type
+ *   `dims->dtype` (bf16 or fp32).  Scores, key means and LSEs are fp32;
+ *   indices are int32.  Arithmetic is fp32 (bf16 inputs feed bf16 matrix
+ *   cores with fp32 accumulation; the attention probabilities are rounded to
+ *   bf16 before the P*V product on the bf16 path and stay fp32 on the fp32
+ *   path).
+ *
+ * Symbols (the paper's problem statement, Section 5): B sequences, N chunks of
+ * C content tokens each with a BOS token prepended, L_q query rows, L_m (= |m|)
+ * pseudo-label rows, L_d decode rows, H_q query heads, H_kv key/value heads
+ * (query head h reads KV head h / (H_q/H_kv)), head dimension d, top-K chunks
+ * and a budget of B_tok tokens per kept chunk.  S_c = 1 + C + L_q + L_m is the
+ * length of one chunk sequence [BOS; c; q; m].
+ */
+#ifndef PD_H
+#define PD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PD_OK = 0,
+  PD_ERR_NULL_PTR = 1,    /* a required pointer is NULL                          */
+  PD_ERR_BAD_DIMS = 2,    /* a size is out of range (see each entry point)       */
+  PD_ERR_UNSUPPORTED = 3, /* H_q % H_kv != 0, d not in {64,128}, unknown dtype    */
+  PD_ERR_MISALIGNED = 4,  /* a pointer is not 16-byte aligned                     */
+  PD_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than pd_workspace_bytes()  */
+  PD_ERR_HIP = 6          /* a kernel launch failed                               */
+} pd_status;
+
+typedef enum { PD_BF16 = 0, PD_FP32 = 1 } pd_dtype;
+
+typedef struct {
+  int32_t batch;        /* B >= 1                                                   */
+  int32_t n_chunks;     /* N, 1..1024                                               */
+  int32_t chunk_len;    /* C, 1..8192 content tokens; the cache holds 1+C rows      */
+  int32_t q_len;        /* L_q >= 1 query rows                                      */
+  int32_t m_len;        /* L_m >= 0 pseudo-label rows                               */
+  int32_t dec_len;      /* L_d >= 1 decode rows                                     */
+  int32_t n_heads_q;    /* H_q >= 1                                                 */
+  int32_t n_heads_kv;   /* H_kv >= 1, divides H_q                                   */
+  int32_t head_dim;     /* d, 64 or 128                                             */
+  int32_t dtype;        /* pd_dtype                                                 */
+  float sm_scale;       /* softmax scale; <= 0 selects 1/sqrt(d)                    */
+  int32_t qm_per_chunk; /* 0: the q/m rows are one tensor shared by all chunks,
+                           [B][L_q+L_m][H][d];  1: one copy per chunk,
+                           [B][N][L_q+L_m][H][d]                                    */
+} pd_dims;
+
+/*
+ * Stage (a), one layer: chunk prefill (Section 5.1, Eq. 2), the chunk KV
+ * cache, the chunk key summary, and the eviction score of Eq. 5 (Section 5.2).
+ *
+ * For every sequence b, chunk n and query head h, the S_c rows
+ * [BOS; c_1..c_C; q_1..q_Lq; m_1..m_Lm] of chunk n attend to each other with
+ * full bidirectional softmax(scale * Q K^T) V and to nothing outside the chunk.
+ *
+ * Inputs (element type dims->dtype):
+ *   q_pre  [B][N][1+C][H_q][d]   chunk rows, slot 0 = the BOS token
+ *   k_pre, v_pre [B][N][1+C][H_kv][d]
+ *   q_qm   query + pseudo-label rows, [B][L_q+L_m][H_q][d] (shared) or
+ *          [B][N][L_q+L_m][H_q][d] (qm_per_chunk = 1); rows 0..L_q-1 are the
+ *          query rows
+ *   k_qm, v_qm  likewise with H_kv heads
+ * Outputs:
+ *   o         [B][N][S_c][H_q][d]   attention output, rows ordered BOS, c, q, m
+ *   k_cache, v_cache [B][N][H_kv][1+C][d]  exact copies of the chunk rows
+ *             (BOS at slot 0), chunk-contiguous per KV head
+ *   tok_score fp32 [B][N][C]  e(c_j) of Eq. 5: for content token j, the
+ *             softmax mass the L_q query rows put on it plus the mass it puts
+ *             on the L_q query columns, summed over all H_q heads
+ *   key_mean  fp32 [B][N][H_kv][d]  mean of the C content keys (BOS excluded)
+ * workspace: >= pd_workspace_bytes(dims, 0, 0, 0, 0) bytes.
+ * Errors: PD_ERR_BAD_DIMS for a size out of range; see the status list.
+ */
+pd_status pd_prefill_chunks(const pd_dims *dims,
+                            const void *q_pre, const void *k_pre, const void *v_pre,
+                            const void *q_qm, const void *k_qm, const void *v_qm,
+                            void *o, void *k_cache, void *v_cache,
+                            float *tok_score, float *key_mean,
+                            void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * Stage (b), one layer, one denoising step: chunk scores, top-K chunks
+ * (Section 5.2, inter-chunk sparsity) and the top-B_tok tokens of each kept
+ * chunk by the Eq. 5 score (intra-chunk sparsity).
+ *
+ * The chunk score is an attention-space stand-in for the paper's NLL score:
+ *   s[b][n] = sum_h scale * < mean_r q_dec[b][r][h], key_mean[b][n][h/G] >,
+ * higher = kept.  Ties rank the lower chunk (token) index first.
+ * Inputs:  q_dec [B][L_d][H_q][d] (dims->dtype), key_mean fp32 [B][N][H_kv][d],
+ *          tok_score fp32 [B][N][C].
+ * Outputs: chunk_idx int32 [B][top_k], ascending chunk indices;
+ *          tok_slot  int32 [B][top_k][tok_budget], ascending cache slots in
+ *          1..C of the kept tokens of chunk chunk_idx[b][k] (slot = token+1);
+ *          chunk_score fp32 [B][N] or NULL.
+ * Sizes: 1 <= top_k <= N, 1 <= tok_budget <= C.
+ * workspace: >= pd_workspace_bytes(dims, top_k, tok_budget, 0, 1) bytes.
+ */
+pd_status pd_score_select(const pd_dims *dims, int32_t top_k, int32_t tok_budget,
+                          const void *q_dec, const float *key_mean, const float *tok_score,
+                          int32_t *chunk_idx, int32_t *tok_slot, float *chunk_score,
+                          void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * Stage (c), one layer, one denoising step: the L_d decode rows attend
+ * (bidirectionally) over, in order, for each kept chunk chunk_idx[b][k]: its
+ * BOS row (cache slot 0) and the rows at slots tok_slot[b][k][*]; then rows
+ * 0..n_static-1 of the static query KV; then their own L_d rows (Section 5.3,
+ * prefix reuse).  L_kv = top_k*(1+tok_budget) + n_static + L_d rows.
+ *
+ * Inputs (dims->dtype): q_dec [B][L_d][H_q][d]; k_dec, v_dec [B][L_d][H_kv][d];
+ *   k_cache, v_cache as written by pd_prefill_chunks; k_static, v_static
+ *   [B][L_q+L_m][H_kv][d] (rows 0..n_static-1 used; may be NULL when
+ *   n_static = 0); chunk_idx, tok_slot as written by pd_score_select (entries
+ *   must lie in 0..N-1 and 1..C).
+ * Outputs: o_dec [B][L_d][H_q][d]; lse_dec fp32 [B][H_q][L_d] natural-log
+ *   row LSE, or NULL.
+ * num_splits: the KV rows are cut into that many shards processed in
+ *   parallel and merged by log-sum-exp (the paper's Split-S); 0 = chosen by the
+ *   library from the sizes; otherwise 1..64.
+ * Sizes: 1 <= top_k <= N, 1 <= tok_budget <= C, 0 <= n_static <= L_q + L_m.
+ * workspace: >= pd_workspace_bytes(dims, top_k, tok_budget, num_splits, 2)
+ *   bytes (may be 0, then workspace may be NULL).
+ */
+pd_status pd_sparse_decode_attn(const pd_dims *dims, int32_t top_k, int32_t tok_budget,
+                                const void *q_dec, const void *k_dec, const void *v_dec,
+                                const void *k_cache, const void *v_cache,
+                                const int32_t *chunk_idx, const int32_t *tok_slot,
+                                const void *k_static, const void *v_static, int32_t n_static,
+                                void *o_dec, float *lse_dec, int32_t num_splits,
+                                void *workspace, size_t ws_bytes, void *stream);
+
+/* Bytes of ONE of k_cache / v_cache for one layer: B*N*H_kv*(1+C)*d*elem. */
+size_t pd_cache_bytes(const pd_dims *dims);
+
+/* Workspace bytes for `which` = 0 prefill, 1 select, 2 decode (num_splits as
+ * passed to pd_sparse_decode_attn; 0 = automatic).  Returns 0 for invalid
+ * dims (the matching entry point then reports the error). */
+size_t pd_workspace_bytes(const pd_dims *dims, int32_t top_k, int32_t tok_budget,
+                          int32_t num_splits, int32_t which);
+
+/* The number of KV shards pd_sparse_decode_attn uses for these arguments. */
+int32_t pd_decode_splits(const pd_dims *dims, int32_t top_k, int32_t tok_budget,
+                         int32_t n_static, int32_t num_splits);
+
+const char *pd_status_string(pd_status s);
+const char *pd_last_error_message(void); /* thread-local detail of the last error */
+const char *pd_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PD_H */

@@ -1,0 +1,167 @@
+"""ctypes binding of ``libpd.so`` (the C ABI declared in include/pd.h).
+
+Argument marshalling only: torch tensors are passed as device pointers, the
+stream as its ``hipStream_t`` handle; every step of the path runs in the HIP
+kernels.  If the library is missing this module raises -- there is no CPU
+fallback.
+"""
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libpd.so")
+
+PD_BF16, PD_FP32 = 0, 1
+STATUS = {0: "PD_OK", 1: "PD_ERR_NULL_PTR", 2: "PD_ERR_BAD_DIMS", 3: "PD_ERR_UNSUPPORTED",
+          4: "PD_ERR_MISALIGNED", 5: "PD_ERR_WORKSPACE", 6: "PD_ERR_HIP"}
+
+EXPORTS = ["pd_prefill_chunks", "pd_score_select", "pd_sparse_decode_attn", "pd_cache_bytes",
+           "pd_workspace_bytes", "pd_decode_splits", "pd_status_string", "pd_last_error_message",
+           "pd_version"]
+
+
+class PdError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+class PdDims(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32), ("n_chunks", ctypes.c_int32), ("chunk_len", ctypes.c_int32),
+        ("q_len", ctypes.c_int32), ("m_len", ctypes.c_int32), ("dec_len", ctypes.c_int32),
+        ("n_heads_q", ctypes.c_int32), ("n_heads_kv", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+        ("dtype", ctypes.c_int32), ("sm_scale", ctypes.c_float), ("qm_per_chunk", ctypes.c_int32),
+    ]
+
+
+@dataclass
+class Dims:
+    """Problem sizes in the paper's notation (Section 5): B, N, C, L_q, L_m, L_d, heads, d."""
+    batch: int
+    n_chunks: int
+    chunk_len: int
+    q_len: int
+    m_len: int
+    dec_len: int
+    n_heads_q: int
+    n_heads_kv: int
+    head_dim: int
+    dtype: int = PD_BF16
+    sm_scale: float = 0.0
+    qm_per_chunk: int = 0
+
+    @property
+    def seq_len(self):
+        """S_c = 1 + C + L_q + L_m, rows of one chunk sequence."""
+        return 1 + self.chunk_len + self.q_len + self.m_len
+
+    def c(self):
+        return PdDims(self.batch, self.n_chunks, self.chunk_len, self.q_len, self.m_len, self.dec_len,
+                      self.n_heads_q, self.n_heads_kv, self.head_dim, self.dtype, self.sm_scale,
+                      self.qm_per_chunk)
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load libpd.so once and declare the signatures; raises if it is not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"HIP library not built: {path} (run __graft_entry__.build())")
+    lib = ctypes.CDLL(path)
+    vp, sz, i32, fp = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_void_p
+    dp = ctypes.POINTER(PdDims)
+    lib.pd_prefill_chunks.argtypes = [dp] + [vp] * 11 + [vp, sz, vp]
+    lib.pd_prefill_chunks.restype = ctypes.c_int
+    lib.pd_score_select.argtypes = [dp, i32, i32, vp, fp, fp, vp, vp, fp, vp, sz, vp]
+    lib.pd_score_select.restype = ctypes.c_int
+    lib.pd_sparse_decode_attn.argtypes = [dp, i32, i32] + [vp] * 9 + [i32, vp, fp, i32, vp, sz, vp]
+    lib.pd_sparse_decode_attn.restype = ctypes.c_int
+    lib.pd_cache_bytes.argtypes = [dp]
+    lib.pd_cache_bytes.restype = sz
+    lib.pd_workspace_bytes.argtypes = [dp, i32, i32, i32, i32]
+    lib.pd_workspace_bytes.restype = sz
+    lib.pd_decode_splits.argtypes = [dp, i32, i32, i32, i32]
+    lib.pd_decode_splits.restype = i32
+    lib.pd_status_string.argtypes = [ctypes.c_int]
+    lib.pd_status_string.restype = ctypes.c_char_p
+    lib.pd_last_error_message.argtypes = []
+    lib.pd_last_error_message.restype = ctypes.c_char_p
+    lib.pd_version.argtypes = []
+    lib.pd_version.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _ptr(t):
+    """Device pointer of a tensor (or None / an int address)."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to the HIP library must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return stream if isinstance(stream, int) else stream.cuda_stream
+
+
+def _check(status):
+    if status != 0:
+        raise PdError(status, load().pd_last_error_message().decode())
+
+
+def _nbytes(t):
+    return 0 if t is None else t.numel() * t.element_size()
+
+
+def pd_cache_bytes(dims: Dims) -> int:
+    return load().pd_cache_bytes(ctypes.byref(dims.c()))
+
+
+def pd_workspace_bytes(dims: Dims, top_k=0, tok_budget=0, num_splits=0, which=0) -> int:
+    return load().pd_workspace_bytes(ctypes.byref(dims.c()), top_k, tok_budget, num_splits, which)
+
+
+def pd_decode_splits(dims: Dims, top_k, tok_budget, n_static, num_splits=0) -> int:
+    return load().pd_decode_splits(ctypes.byref(dims.c()), top_k, tok_budget, n_static, num_splits)
+
+
+def pd_prefill_chunks(dims: Dims, q_pre, k_pre, v_pre, q_qm, k_qm, v_qm, o, k_cache, v_cache,
+                      tok_score, key_mean, workspace, stream=None):
+    """Stage (a) for one layer (see include/pd.h)."""
+    _check(load().pd_prefill_chunks(
+        ctypes.byref(dims.c()), _ptr(q_pre), _ptr(k_pre), _ptr(v_pre), _ptr(q_qm), _ptr(k_qm), _ptr(v_qm),
+        _ptr(o), _ptr(k_cache), _ptr(v_cache), _ptr(tok_score), _ptr(key_mean),
+        _ptr(workspace), _nbytes(workspace), _stream(stream)))
+
+
+def pd_score_select(dims: Dims, top_k, tok_budget, q_dec, key_mean, tok_score, chunk_idx, tok_slot,
+                    chunk_score, workspace, stream=None):
+    """Stage (b) for one layer and step (see include/pd.h)."""
+    _check(load().pd_score_select(
+        ctypes.byref(dims.c()), top_k, tok_budget, _ptr(q_dec), _ptr(key_mean), _ptr(tok_score),
+        _ptr(chunk_idx), _ptr(tok_slot), _ptr(chunk_score), _ptr(workspace), _nbytes(workspace),
+        _stream(stream)))
+
+
+def pd_sparse_decode_attn(dims: Dims, top_k, tok_budget, q_dec, k_dec, v_dec, k_cache, v_cache,
+                          chunk_idx, tok_slot, k_static, v_static, n_static, o_dec, lse_dec,
+                          num_splits, workspace, stream=None):
+    """Stage (c) for one layer and step (see include/pd.h)."""
+    _check(load().pd_sparse_decode_attn(
+        ctypes.byref(dims.c()), top_k, tok_budget, _ptr(q_dec), _ptr(k_dec), _ptr(v_dec),
+        _ptr(k_cache), _ptr(v_cache), _ptr(chunk_idx), _ptr(tok_slot), _ptr(k_static), _ptr(v_static),
+        n_static, _ptr(o_dec), _ptr(lse_dec), num_splits, _ptr(workspace), _nbytes(workspace),
+        _stream(stream)))

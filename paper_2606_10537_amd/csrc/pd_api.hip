@@ -1,0 +1,401 @@
+// C-ABI entry points: argument validation, workspace layout, launches.
+// Everything here runs on the host; kernels are enqueued on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "pd.h"
+#include "pd_kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+pd_status fail(pd_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+pd_status ok() {
+  g_last_error.clear();
+  return PD_OK;
+}
+
+constexpr int kMaxChunks = 1024;
+constexpr int kMaxChunkLen = 4096;
+constexpr int kMaxSplits = 64;
+constexpr int kTargetWorkgroups = 512;  // two resident workgroups per CU on 256 CUs
+constexpr size_t kAlign = 256;
+
+size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+pd_status check_dims(const pd_dims* d) {
+  if (!d) return fail(PD_ERR_NULL_PTR, "dims is NULL");
+  if (d->batch < 1) return fail(PD_ERR_BAD_DIMS, "batch=%d must be >= 1", d->batch);
+  if (d->n_chunks < 1 || d->n_chunks > kMaxChunks)
+    return fail(PD_ERR_BAD_DIMS, "n_chunks=%d must be in 1..%d", d->n_chunks, kMaxChunks);
+  if (d->chunk_len < 1 || d->chunk_len > kMaxChunkLen)
+    return fail(PD_ERR_BAD_DIMS, "chunk_len=%d must be in 1..%d", d->chunk_len, kMaxChunkLen);
+  if (d->q_len < 1) return fail(PD_ERR_BAD_DIMS, "q_len=%d must be >= 1", d->q_len);
+  if (d->m_len < 0) return fail(PD_ERR_BAD_DIMS, "m_len=%d must be >= 0", d->m_len);
+  if (d->dec_len < 1) return fail(PD_ERR_BAD_DIMS, "dec_len=%d must be >= 1", d->dec_len);
+  if (d->n_heads_q < 1 || d->n_heads_kv < 1)
+    return fail(PD_ERR_BAD_DIMS, "head counts %d/%d must be >= 1", d->n_heads_q, d->n_heads_kv);
+  if (d->qm_per_chunk != 0 && d->qm_per_chunk != 1)
+    return fail(PD_ERR_BAD_DIMS, "qm_per_chunk=%d must be 0 or 1", d->qm_per_chunk);
+  if (d->n_heads_q % d->n_heads_kv != 0)
+    return fail(PD_ERR_UNSUPPORTED, "n_heads_q=%d is not a multiple of n_heads_kv=%d", d->n_heads_q, d->n_heads_kv);
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(PD_ERR_UNSUPPORTED, "head_dim=%d must be 64 or 128", d->head_dim);
+  if (d->dtype != PD_BF16 && d->dtype != PD_FP32)
+    return fail(PD_ERR_UNSUPPORTED, "dtype=%d is neither PD_BF16 nor PD_FP32", d->dtype);
+  if (!(std::isfinite(d->sm_scale))) return fail(PD_ERR_BAD_DIMS, "sm_scale is not finite");
+  const long long sc = 1LL + d->chunk_len + d->q_len + d->m_len;
+  if (sc > (1LL << 24) || d->dec_len > (1 << 24))
+    return fail(PD_ERR_BAD_DIMS, "sequence length too large");
+  // Grid sizes must fit one launch dimension.
+  const long long grid = (long long)d->batch * d->n_chunks * d->n_heads_q * cdiv(sc, 64);
+  if (grid >= (1LL << 31)) return fail(PD_ERR_BAD_DIMS, "problem too large for one launch");
+  return PD_OK;
+}
+
+int elem_bytes(const pd_dims* d) { return d->dtype == PD_BF16 ? 2 : 4; }
+float scale_of(const pd_dims* d) { return d->sm_scale > 0.f ? d->sm_scale : 1.0f / std::sqrt((float)d->head_dim); }
+
+// --- workspace layouts -------------------------------------------------------
+struct PrefillWs {
+  size_t part_i, lse_q, total;
+};
+PrefillWs prefill_ws(const pd_dims* d) {
+  PrefillWs w;
+  const size_t bnh = (size_t)d->batch * d->n_chunks * d->n_heads_q;
+  w.part_i = 0;
+  w.lse_q = round_up(bnh * d->chunk_len * sizeof(float));
+  w.total = w.lse_q + round_up(bnh * d->q_len * sizeof(float));
+  return w;
+}
+
+struct SelectWs {
+  size_t qbar, scores, total;
+};
+SelectWs select_ws(const pd_dims* d) {
+  SelectWs w;
+  w.qbar = 0;
+  w.scores = round_up((size_t)d->batch * d->n_heads_q * d->head_dim * sizeof(float));
+  w.total = w.scores + round_up((size_t)d->batch * d->n_chunks * sizeof(float));
+  return w;
+}
+
+int decode_qtiles(const pd_dims* d) {
+  const int G = d->n_heads_q / d->n_heads_kv;
+  return d->dtype == PD_BF16 ? cdiv((long long)G * d->dec_len, 128) : cdiv(d->dec_len, 64);
+}
+int decode_units(const pd_dims* d) {
+  return d->dtype == PD_BF16 ? d->batch * d->n_heads_kv * decode_qtiles(d)
+                             : d->batch * d->n_heads_q * decode_qtiles(d);
+}
+
+// Requested shard count: explicit, or chosen so that the decode grid reaches
+// about two workgroups per CU while every shard keeps >= 4 KV tiles of 64 rows.
+int requested_splits(const pd_dims* d, int top_k, int tok_budget, int num_splits) {
+  if (num_splits > 0) return num_splits;
+  const long long lkv0 = (long long)top_k * (1 + tok_budget) + d->dec_len;
+  const int max_by_len = std::max(1, cdiv(lkv0, 64) / 4);
+  const int want = cdiv(kTargetWorkgroups, std::max(1, decode_units(d)));
+  return std::max(1, std::min(std::min(want, max_by_len), kMaxSplits));
+}
+
+int effective_splits(const pd_dims* d, int top_k, int tok_budget, int n_static, int num_splits) {
+  const long long lkv = (long long)top_k * (1 + tok_budget) + n_static + d->dec_len;
+  const int tile = d->dtype == PD_BF16 ? 64 : 32;
+  return std::max(1, std::min(requested_splits(d, top_k, tok_budget, num_splits), cdiv(lkv, tile)));
+}
+
+size_t decode_ws_bytes(const pd_dims* d, int S) {
+  if (S <= 1) return 0;
+  const size_t rows = (size_t)S * d->batch * d->n_heads_q * d->dec_len;
+  return round_up(rows * d->head_dim * sizeof(float)) + round_up(rows * sizeof(float));
+}
+
+pd_status check_ws(void* ws, size_t have, size_t need) {
+  if (need == 0) return PD_OK;
+  if (!ws) return fail(PD_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed", need);
+  if (!aligned16(ws)) return fail(PD_ERR_MISALIGNED, "workspace is not 16-byte aligned");
+  if (have < need) return fail(PD_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", have, need);
+  return PD_OK;
+}
+
+#define PD_REQUIRE_PTR(p)                                               \
+  do {                                                                  \
+    if (!(p)) return fail(PD_ERR_NULL_PTR, "pointer '%s' is NULL", #p); \
+    if (!aligned16(p)) return fail(PD_ERR_MISALIGNED, "pointer '%s' is not 16-byte aligned", #p); \
+  } while (0)
+
+#define PD_RETURN_IF(st)          \
+  do {                            \
+    pd_status _s = (st);          \
+    if (_s != PD_OK) return _s;   \
+  } while (0)
+
+pd_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(PD_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* pd_version(void) { return "pd-mi355x 0.1 (gfx950)"; }
+
+const char* pd_status_string(pd_status s) {
+  switch (s) {
+    case PD_OK: return "PD_OK";
+    case PD_ERR_NULL_PTR: return "PD_ERR_NULL_PTR";
+    case PD_ERR_BAD_DIMS: return "PD_ERR_BAD_DIMS";
+    case PD_ERR_UNSUPPORTED: return "PD_ERR_UNSUPPORTED";
+    case PD_ERR_MISALIGNED: return "PD_ERR_MISALIGNED";
+    case PD_ERR_WORKSPACE: return "PD_ERR_WORKSPACE";
+    case PD_ERR_HIP: return "PD_ERR_HIP";
+  }
+  return "PD_ERR_UNKNOWN";
+}
+
+const char* pd_last_error_message(void) { return g_last_error.c_str(); }
+
+size_t pd_cache_bytes(const pd_dims* d) {
+  if (check_dims(d) != PD_OK) return 0;
+  return (size_t)d->batch * d->n_chunks * d->n_heads_kv * (d->chunk_len + 1) * d->head_dim * elem_bytes(d);
+}
+
+size_t pd_workspace_bytes(const pd_dims* d, int32_t top_k, int32_t tok_budget, int32_t num_splits, int32_t which) {
+  if (check_dims(d) != PD_OK) return 0;
+  switch (which) {
+    case 0: return prefill_ws(d).total;
+    case 1: return select_ws(d).total;
+    case 2:
+      if (top_k < 1 || tok_budget < 1 || num_splits < 0 || num_splits > kMaxSplits) return 0;
+      return decode_ws_bytes(d, requested_splits(d, top_k, tok_budget, num_splits));
+    default: return 0;
+  }
+}
+
+int32_t pd_decode_splits(const pd_dims* d, int32_t top_k, int32_t tok_budget, int32_t n_static, int32_t num_splits) {
+  if (check_dims(d) != PD_OK || top_k < 1 || tok_budget < 1 || num_splits < 0 || num_splits > kMaxSplits) return 0;
+  return effective_splits(d, top_k, tok_budget, n_static, num_splits);
+}
+
+pd_status pd_prefill_chunks(const pd_dims* d, const void* q_pre, const void* k_pre, const void* v_pre,
+                            const void* q_qm, const void* k_qm, const void* v_qm, void* o, void* k_cache,
+                            void* v_cache, float* tok_score, float* key_mean, void* workspace, size_t ws_bytes,
+                            void* stream) {
+  PD_RETURN_IF(check_dims(d));
+  PD_REQUIRE_PTR(q_pre);
+  PD_REQUIRE_PTR(k_pre);
+  PD_REQUIRE_PTR(v_pre);
+  PD_REQUIRE_PTR(q_qm);
+  PD_REQUIRE_PTR(k_qm);
+  PD_REQUIRE_PTR(v_qm);
+  PD_REQUIRE_PTR(o);
+  PD_REQUIRE_PTR(k_cache);
+  PD_REQUIRE_PTR(v_cache);
+  PD_REQUIRE_PTR(tok_score);
+  PD_REQUIRE_PTR(key_mean);
+  const PrefillWs w = prefill_ws(d);
+  PD_RETURN_IF(check_ws(workspace, ws_bytes, w.total));
+
+  hipStream_t s = (hipStream_t)stream;
+  const bool bf16 = d->dtype == PD_BF16;
+  char* ws = (char*)workspace;
+  pd::PrefillArgs a{};
+  a.q_pre = (const uint16_t*)q_pre;
+  a.k_pre = (const uint16_t*)k_pre;
+  a.v_pre = (const uint16_t*)v_pre;
+  a.q_qm = (const uint16_t*)q_qm;
+  a.k_qm = (const uint16_t*)k_qm;
+  a.v_qm = (const uint16_t*)v_qm;
+  a.o = (uint16_t*)o;
+  a.k_cache = (uint16_t*)k_cache;
+  a.v_cache = (uint16_t*)v_cache;
+  a.part_i = (float*)(ws + w.part_i);
+  a.lse_q = (float*)(ws + w.lse_q);
+  a.B = d->batch;
+  a.N = d->n_chunks;
+  a.C = d->chunk_len;
+  a.Lq = d->q_len;
+  a.Lm = d->m_len;
+  a.Hq = d->n_heads_q;
+  a.Hkv = d->n_heads_kv;
+  a.G = a.Hq / a.Hkv;
+  a.Sc = 1 + a.C + a.Lq + a.Lm;
+  a.qm_per_chunk = d->qm_per_chunk;
+  a.scale_log2 = scale_of(d) * 1.4426950408889634f;
+  a.n_qt = cdiv(a.Sc, bf16 ? 128 : 64);
+  a.n_kvt = cdiv(a.Sc, 64);
+  a.total = a.B * a.N * a.Hq * a.n_qt;
+
+  pd::EscoreArgs e{};
+  e.q_qm = a.q_qm;
+  e.k_cache = a.k_cache;
+  e.part_i = a.part_i;
+  e.lse_q = a.lse_q;
+  e.tok_score = tok_score;
+  e.B = a.B;
+  e.N = a.N;
+  e.C = a.C;
+  e.Lq = a.Lq;
+  e.Lm = a.Lm;
+  e.Hq = a.Hq;
+  e.Hkv = a.Hkv;
+  e.G = a.G;
+  e.n_cb = cdiv(a.C, 64);
+  e.total = a.B * a.N * e.n_cb;
+  e.qm_per_chunk = a.qm_per_chunk;
+  e.scale_log2 = a.scale_log2;
+
+  hipError_t err;
+  if (bf16) {
+    err = pd::launch_prefill_bf16(a, d->head_dim, s);
+    if (err != hipSuccess) return hip_status(err, "prefill kernel");
+    err = pd::launch_escore_bf16(e, d->head_dim, s);
+    if (err != hipSuccess) return hip_status(err, "token-score kernel");
+  } else {
+    err = pd::launch_prefill_f32(a, d->head_dim, s);
+    if (err != hipSuccess) return hip_status(err, "prefill kernel");
+    err = pd::launch_cache_copy(k_pre, v_pre, k_cache, v_cache, a.B, a.N, a.C, a.Hkv, d->head_dim, 4, s);
+    if (err != hipSuccess) return hip_status(err, "cache copy kernel");
+    err = pd::launch_escore_f32(e, d->head_dim, s);
+    if (err != hipSuccess) return hip_status(err, "token-score kernel");
+  }
+  err = pd::launch_key_mean(k_cache, key_mean, a.B, a.N, a.C, a.Hkv, d->head_dim, bf16, s);
+  return hip_status(err, "key-mean kernel");
+}
+
+pd_status pd_score_select(const pd_dims* d, int32_t top_k, int32_t tok_budget, const void* q_dec,
+                          const float* key_mean, const float* tok_score, int32_t* chunk_idx, int32_t* tok_slot,
+                          float* chunk_score, void* workspace, size_t ws_bytes, void* stream) {
+  PD_RETURN_IF(check_dims(d));
+  if (top_k < 1 || top_k > d->n_chunks)
+    return fail(PD_ERR_BAD_DIMS, "top_k=%d must be in 1..n_chunks=%d", top_k, d->n_chunks);
+  if (tok_budget < 1 || tok_budget > d->chunk_len)
+    return fail(PD_ERR_BAD_DIMS, "tok_budget=%d must be in 1..chunk_len=%d", tok_budget, d->chunk_len);
+  PD_REQUIRE_PTR(q_dec);
+  PD_REQUIRE_PTR(key_mean);
+  PD_REQUIRE_PTR(tok_score);
+  PD_REQUIRE_PTR(chunk_idx);
+  PD_REQUIRE_PTR(tok_slot);
+  if (chunk_score && !aligned16(chunk_score))
+    return fail(PD_ERR_MISALIGNED, "pointer 'chunk_score' is not 16-byte aligned");
+  const SelectWs w = select_ws(d);
+  PD_RETURN_IF(check_ws(workspace, ws_bytes, w.total));
+  char* ws = (char*)workspace;
+  pd::SelectArgs a{};
+  a.q_dec = q_dec;
+  a.key_mean = key_mean;
+  a.tok_score = tok_score;
+  a.qbar = (float*)(ws + w.qbar);
+  a.scores = chunk_score ? chunk_score : (float*)(ws + w.scores);
+  a.chunk_idx = chunk_idx;
+  a.tok_slot = tok_slot;
+  a.B = d->batch;
+  a.N = d->n_chunks;
+  a.C = d->chunk_len;
+  a.Hq = d->n_heads_q;
+  a.Hkv = d->n_heads_kv;
+  a.G = a.Hq / a.Hkv;
+  a.Ld = d->dec_len;
+  a.D = d->head_dim;
+  a.K = top_k;
+  a.Bt = tok_budget;
+  a.bf16 = d->dtype == PD_BF16;
+  a.scale = scale_of(d);
+  return hip_status(pd::launch_score_select(a, (hipStream_t)stream), "score/select kernels");
+}
+
+pd_status pd_sparse_decode_attn(const pd_dims* d, int32_t top_k, int32_t tok_budget, const void* q_dec,
+                                const void* k_dec, const void* v_dec, const void* k_cache, const void* v_cache,
+                                const int32_t* chunk_idx, const int32_t* tok_slot, const void* k_static,
+                                const void* v_static, int32_t n_static, void* o_dec, float* lse_dec,
+                                int32_t num_splits, void* workspace, size_t ws_bytes, void* stream) {
+  PD_RETURN_IF(check_dims(d));
+  if (top_k < 1 || top_k > d->n_chunks)
+    return fail(PD_ERR_BAD_DIMS, "top_k=%d must be in 1..n_chunks=%d", top_k, d->n_chunks);
+  if (tok_budget < 1 || tok_budget > d->chunk_len)
+    return fail(PD_ERR_BAD_DIMS, "tok_budget=%d must be in 1..chunk_len=%d", tok_budget, d->chunk_len);
+  if (n_static < 0 || n_static > d->q_len + d->m_len)
+    return fail(PD_ERR_BAD_DIMS, "n_static=%d must be in 0..q_len+m_len=%d", n_static, d->q_len + d->m_len);
+  if (num_splits < 0 || num_splits > kMaxSplits)
+    return fail(PD_ERR_BAD_DIMS, "num_splits=%d must be in 0..%d", num_splits, kMaxSplits);
+  PD_REQUIRE_PTR(q_dec);
+  PD_REQUIRE_PTR(k_dec);
+  PD_REQUIRE_PTR(v_dec);
+  PD_REQUIRE_PTR(k_cache);
+  PD_REQUIRE_PTR(v_cache);
+  PD_REQUIRE_PTR(chunk_idx);
+  PD_REQUIRE_PTR(tok_slot);
+  PD_REQUIRE_PTR(o_dec);
+  if (n_static > 0) {
+    PD_REQUIRE_PTR(k_static);
+    PD_REQUIRE_PTR(v_static);
+  }
+  if (lse_dec && !aligned16(lse_dec)) return fail(PD_ERR_MISALIGNED, "pointer 'lse_dec' is not 16-byte aligned");
+  const int S_req = requested_splits(d, top_k, tok_budget, num_splits);
+  const int S = effective_splits(d, top_k, tok_budget, n_static, num_splits);
+  PD_RETURN_IF(check_ws(workspace, ws_bytes, decode_ws_bytes(d, S_req)));
+
+  const bool bf16 = d->dtype == PD_BF16;
+  hipStream_t s = (hipStream_t)stream;
+  pd::DecodeArgs a{};
+  a.q_dec = (const uint16_t*)q_dec;
+  a.k_dec = (const uint16_t*)k_dec;
+  a.v_dec = (const uint16_t*)v_dec;
+  a.k_cache = (const uint16_t*)k_cache;
+  a.v_cache = (const uint16_t*)v_cache;
+  a.k_static = (const uint16_t*)k_static;
+  a.v_static = (const uint16_t*)v_static;
+  a.chunk_idx = chunk_idx;
+  a.tok_slot = tok_slot;
+  a.o_dec = o_dec;
+  a.lse_dec = lse_dec;
+  a.B = d->batch;
+  a.N = d->n_chunks;
+  a.C = d->chunk_len;
+  a.Hq = d->n_heads_q;
+  a.Hkv = d->n_heads_kv;
+  a.G = a.Hq / a.Hkv;
+  a.Ld = d->dec_len;
+  a.Ls = d->q_len + d->m_len;
+  a.K = top_k;
+  a.Bt = tok_budget;
+  a.n_static = n_static;
+  a.S = S;
+  a.scale_log2 = scale_of(d) * 1.4426950408889634f;
+  a.n_qt = decode_qtiles(d);
+  a.total = decode_units(d) * S;
+  if (S > 1) {
+    const size_t rows = (size_t)S * a.B * a.Hq * a.Ld;
+    a.o_part = (float*)workspace;
+    a.lse_part = (float*)((char*)workspace + round_up(rows * d->head_dim * sizeof(float)));
+  }
+  hipError_t err = bf16 ? pd::launch_decode_bf16(a, d->head_dim, s) : pd::launch_decode_f32(a, d->head_dim, s);
+  if (err != hipSuccess) return hip_status(err, "decode kernel");
+  if (S > 1) {
+    err = pd::launch_merge(a.o_part, a.lse_part, o_dec, lse_dec, S, a.B, a.Hq, a.Ld, d->head_dim, bf16, s);
+    if (err != hipSuccess) return hip_status(err, "merge kernel");
+  }
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,71 @@
+// Kernel argument blocks and launchers (internal to the library).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pd {
+
+// Stage (a).  Element pointers are bf16 bit patterns (uint16_t) or fp32.
+struct PrefillArgs {
+  const uint16_t *q_pre, *k_pre, *v_pre, *q_qm, *k_qm, *v_qm;
+  uint16_t *o, *k_cache, *v_cache;
+  float* part_i;   // [B][N][Hq][C]  per-head mass of content row j on the query columns
+  float* lse_q;    // [B][N][Hq][Lq] log2-domain LSE of the query rows
+  int B, N, C, Lq, Lm, Hq, Hkv, G, Sc;
+  int n_qt, n_kvt, total;
+  int qm_per_chunk;
+  float scale_log2;  // softmax scale * log2(e)
+};
+
+struct EscoreArgs {
+  const uint16_t *q_qm, *k_cache;
+  const float *part_i, *lse_q;
+  float* tok_score;
+  int B, N, C, Lq, Lm, Hq, Hkv, G, n_cb, total, qm_per_chunk;
+  float scale_log2;
+};
+
+// Stage (c).
+struct DecodeArgs {
+  const uint16_t *q_dec, *k_dec, *v_dec, *k_cache, *v_cache, *k_static, *v_static;
+  const int32_t *chunk_idx, *tok_slot;
+  void* o_dec;       // element type of the call
+  float* lse_dec;    // natural-log LSE or nullptr (only when S == 1)
+  float* o_part;     // [S][B][Hq][Ld][D] shard outputs (normalised), S > 1
+  float* lse_part;   // [S][B][Hq][Ld] log2-domain shard LSE, S > 1
+  int B, N, C, Hq, Hkv, G, Ld, Ls, K, Bt, n_static, S;
+  int n_qt, total;
+  float scale_log2;
+};
+
+hipError_t launch_prefill_bf16(const PrefillArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_escore_bf16(const EscoreArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_decode_bf16(const DecodeArgs& a, int head_dim, hipStream_t s);
+
+hipError_t launch_prefill_f32(const PrefillArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_escore_f32(const EscoreArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_decode_f32(const DecodeArgs& a, int head_dim, hipStream_t s);
+
+// Generic (both element types).
+// Chunk cache copy (fp32 path; the bf16 prefill writes the cache itself).
+hipError_t launch_cache_copy(const void* k_pre, const void* v_pre, void* k_cache, void* v_cache,
+                             int B, int N, int C, int Hkv, int head_dim, int elem_bytes, hipStream_t s);
+hipError_t launch_key_mean(const void* k_cache, float* key_mean, int B, int N, int C, int Hkv,
+                           int head_dim, bool bf16, hipStream_t s);
+hipError_t launch_merge(const float* o_part, const float* lse_part, void* o_dec, float* lse_dec,
+                        int S, int B, int Hq, int Ld, int head_dim, bool bf16, hipStream_t s);
+
+// Stage (b).
+struct SelectArgs {
+  const void* q_dec;
+  const float *key_mean, *tok_score;
+  float* qbar;      // [B][Hq][D] workspace
+  float* scores;    // [B][N]
+  int32_t *chunk_idx, *tok_slot;
+  int B, N, C, Hq, Hkv, G, Ld, D, K, Bt;
+  bool bf16;
+  float scale;
+};
+hipError_t launch_score_select(const SelectArgs& a, hipStream_t s);
+
+}  // namespace pd

@@ -1,0 +1,291 @@
+// Stage (b): per-step chunk scores, top-K chunks and top-B_tok tokens per kept
+// chunk.  Three launches:
+//   1. qbar:   grid (b, h)  -- mean decode query of each head (fp32);
+//   2. scores: grid (b, n)  -- s[b][n] = scale * sum_h <qbar[b][h], key_mean[b][n][h/G]>;
+//   3. select: grid (b, k)  -- every workgroup ranks the N chunk scores (bitonic
+//      sort of (score desc, index asc) keys in LDS), takes the k-th kept chunk in
+//      ascending index order, ranks its C token scores the same way and writes
+//      the kept slots in ascending order (flags + block scan).
+// All reductions run in a fixed order, so results are bitwise reproducible.
+#include "pd_common.h"
+#include "pd_kernels.h"
+
+namespace pd {
+
+// 16 bytes of elements as floats: 8 bf16 or 4 fp32.
+template <bool BF16>
+struct Vec16 {
+  static constexpr int E = BF16 ? 8 : 4;
+  __device__ static void load(const void* base, size_t elem_off, float (&v)[E]) {
+    const u32x4 w = *reinterpret_cast<const u32x4*>(
+        reinterpret_cast<const char*>(base) + elem_off * (BF16 ? 2 : 4));
+    if constexpr (BF16) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        v[2 * i] = __uint_as_float(w[i] << 16);
+        v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = __uint_as_float(w[i]);
+    }
+  }
+};
+
+// Sum of `nrows` rows (stride `row_stride` elements) of D elements each,
+// starting at element `base_off`; returns the D sums * `mul` into out[0..D).
+// 256 threads: thread t reads 16-byte chunk (t % TPR) of rows t/TPR, +NG, ...
+template <bool BF16>
+__device__ void rows_mean(const void* src, size_t base_off, size_t row_stride, int nrows, int D,
+                          float mul, float* out, float* red /* [256/TPR][D] */) {
+  constexpr int E = Vec16<BF16>::E;
+  const int TPR = D / E, NG = 256 / TPR;
+  const int t = threadIdx.x, c = t % TPR, rg = t / TPR;
+  float acc[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] = 0.f;
+  for (int r = rg; r < nrows; r += NG) {
+    float v[E];
+    Vec16<BF16>::load(src, base_off + (size_t)r * row_stride + c * E, v);
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] += v[e];
+  }
+#pragma unroll
+  for (int e = 0; e < E; ++e) red[rg * D + c * E + e] = acc[e];
+  __syncthreads();
+  if (t < D) {
+    float s = 0.f;
+    for (int g = 0; g < NG; ++g) s += red[g * D + t];
+    out[t] = s * mul;
+  }
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void qbar_kernel(const void* q_dec, float* qbar, int Ld, int Hq, int D) {
+  __shared__ float red[2048];  // >= (256 / TPR) * D for d <= 128
+  const int b = blockIdx.x / Hq, h = blockIdx.x % Hq;
+  rows_mean<BF16>(q_dec, ((size_t)b * Ld * Hq + h) * D, (size_t)Hq * D, Ld, D, 1.0f / Ld,
+                  qbar + ((size_t)b * Hq + h) * D, red);
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void key_mean_kernel(const void* k_cache, float* key_mean, int C, int D) {
+  __shared__ float red[2048];
+  const size_t bng = blockIdx.x;  // ((b*N + n)*Hkv + g)
+  rows_mean<BF16>(k_cache, (bng * (C + 1) + 1) * D, (size_t)D, C, D, 1.0f / C, key_mean + bng * D, red);
+}
+
+__global__ __launch_bounds__(256) void chunk_score_kernel(const float* qbar, const float* key_mean,
+                                                           float* scores, int N, int Hq, int Hkv,
+                                                           int G, int D, float scale) {
+  __shared__ float red[256];
+  const int b = blockIdx.x / N, n = blockIdx.x % N;
+  const float* qb = qbar + (size_t)b * Hq * D;
+  const float* kb = key_mean + ((size_t)b * N + n) * Hkv * D;
+  float acc = 0.f;
+  for (int i = threadIdx.x; i < Hq * D; i += 256) {
+    const int h = i / D, dd = i - h * D;
+    acc += qb[i] * kb[(h / G) * D + dd];
+  }
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) scores[(size_t)b * N + n] = red[0] * scale;
+}
+
+__device__ __forceinline__ uint64_t rank_key(float score, int idx) {
+  return ((uint64_t)(~float_order_key(score)) << 32) | (uint32_t)idx;
+}
+
+// Ascending bitonic sort of P (power of two) keys in LDS, 256 threads.
+__device__ void bitonic_sort(uint64_t* keys, int P) {
+  for (int k = 2; k <= P; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = threadIdx.x; i < P; i += 256) {
+        const int ixj = i ^ j;
+        if (ixj > i) {
+          const uint64_t a = keys[i], c = keys[ixj];
+          const bool up = (i & k) == 0;
+          if ((a > c) == up) {
+            keys[i] = c;
+            keys[ixj] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void select_kernel(const float* scores, const float* tok_score,
+                                                      int32_t* chunk_idx, int32_t* tok_slot, int N,
+                                                      int C, int K, int Bt, int Npad, int Cpad) {
+  extern __shared__ __attribute__((aligned(16))) uint64_t sh[];
+  __shared__ int my_chunk;
+  __shared__ int scan[2][256];
+  const int P = Npad > Cpad ? Npad : Cpad;
+  uint64_t* keys = sh;
+  int* flag = reinterpret_cast<int*>(sh + P);
+  const int b = blockIdx.x / K, k = blockIdx.x % K;
+  const int t = threadIdx.x;
+
+  // Top-K chunks.
+  for (int i = t; i < Npad; i += 256) keys[i] = i < N ? rank_key(scores[(size_t)b * N + i], i) : ~0ull;
+  __syncthreads();
+  bitonic_sort(keys, Npad);
+  for (int i = t; i < K; i += 256) {
+    const int x = (int)(uint32_t)keys[i];
+    int pos = 0;
+    for (int j = 0; j < K; ++j) pos += (int)(uint32_t)keys[j] < x;
+    if (pos == k) my_chunk = x;
+    if (k == 0) chunk_idx[(size_t)b * K + pos] = x;
+  }
+  __syncthreads();
+  const int n = my_chunk;
+  __syncthreads();
+
+  // Top-Bt tokens of chunk n.
+  const float* e = tok_score + ((size_t)b * N + n) * C;
+  for (int j = t; j < Cpad; j += 256) {
+    keys[j] = j < C ? rank_key(e[j], j) : ~0ull;
+    flag[j] = 0;
+  }
+  __syncthreads();
+  bitonic_sort(keys, Cpad);
+  for (int i = t; i < Bt; i += 256) flag[(uint32_t)keys[i]] = 1;
+  __syncthreads();
+
+  // Exclusive scan of the flags over contiguous segments of C.
+  const int seg = (C + 255) / 256;
+  const int j0 = t * seg, j1 = min(C, j0 + seg);
+  int cnt = 0;
+  for (int j = j0; j < j1; ++j) cnt += flag[j];
+  scan[0][t] = cnt;
+  __syncthreads();
+  int cur = 0;
+  for (int w = 1; w < 256; w <<= 1) {
+    const int v = scan[cur][t] + (t >= w ? scan[cur][t - w] : 0);
+    scan[cur ^ 1][t] = v;
+    cur ^= 1;
+    __syncthreads();
+  }
+  int pos = scan[cur][t] - cnt;
+  int32_t* out = tok_slot + ((size_t)b * K + k) * Bt;
+  for (int j = j0; j < j1; ++j)
+    if (flag[j]) out[pos++] = j + 1;
+}
+
+static int next_pow2(int x) {
+  int p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+hipError_t launch_score_select(const SelectArgs& a, hipStream_t s) {
+  if (a.bf16)
+    hipLaunchKernelGGL(qbar_kernel<true>, dim3(a.B * a.Hq), dim3(256), 0, s, a.q_dec, a.qbar, a.Ld, a.Hq, a.D);
+  else
+    hipLaunchKernelGGL(qbar_kernel<false>, dim3(a.B * a.Hq), dim3(256), 0, s, a.q_dec, a.qbar, a.Ld, a.Hq, a.D);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(chunk_score_kernel, dim3(a.B * a.N), dim3(256), 0, s, a.qbar, a.key_mean, a.scores,
+                     a.N, a.Hq, a.Hkv, a.G, a.D, a.scale);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  const int Npad = next_pow2(a.N), Cpad = next_pow2(a.C);
+  const int P = Npad > Cpad ? Npad : Cpad;
+  const size_t lds = (size_t)P * 8 + (size_t)P * 4;
+  hipLaunchKernelGGL(select_kernel, dim3(a.B * a.K), dim3(256), lds, s, a.scores, a.tok_score, a.chunk_idx,
+                     a.tok_slot, a.N, a.C, a.K, a.Bt, Npad, Cpad);
+  return hipGetLastError();
+}
+
+hipError_t launch_key_mean(const void* k_cache, float* key_mean, int B, int N, int C, int Hkv, int head_dim,
+                           bool bf16, hipStream_t s) {
+  if (bf16)
+    hipLaunchKernelGGL(key_mean_kernel<true>, dim3(B * N * Hkv), dim3(256), 0, s, k_cache, key_mean, C, head_dim);
+  else
+    hipLaunchKernelGGL(key_mean_kernel<false>, dim3(B * N * Hkv), dim3(256), 0, s, k_cache, key_mean, C, head_dim);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Split-S merge: O = sum_s 2^(lse_s - M) O_s / sum_s 2^(lse_s - M).
+template <bool BF16>
+__global__ __launch_bounds__(256) void merge_kernel(const float* o_part, const float* lse_part, void* o_dec,
+                                                     float* lse_dec, int S, int B, int Hq, int Ld, int D) {
+  const int TPR = D / 4;
+  const size_t gid = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const size_t rows = (size_t)B * Hq * Ld;
+  const size_t row = gid / TPR;
+  if (row >= rows) return;
+  const int c = gid % TPR;
+  float M = -INFINITY;
+  for (int sp = 0; sp < S; ++sp) M = fmaxf(M, lse_part[sp * rows + row]);
+  float W = 0.f;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int sp = 0; sp < S; ++sp) {
+    const float w = fast_exp2(lse_part[sp * rows + row] - M);
+    W += w;
+    const f32x4 v = *reinterpret_cast<const f32x4*>(o_part + (sp * rows + row) * D + 4 * c);
+    acc += w * v;
+  }
+  const float inv = 1.0f / W;
+  // row = (b*Hq + h)*Ld + r  ->  o_dec[b][r][h][:]
+  const int r = row % Ld;
+  const size_t bh = row / Ld;
+  const int h = bh % Hq;
+  const size_t b = bh / Hq;
+  const size_t out = ((b * Ld + r) * Hq + h) * D + 4 * c;
+  if constexpr (BF16) {
+    u32x2 v = {pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv)};
+    *reinterpret_cast<u32x2*>(reinterpret_cast<uint16_t*>(o_dec) + out) = v;
+  } else {
+    *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(o_dec) + out) = acc * inv;
+  }
+  if (lse_dec && c == 0) lse_dec[row] = (M + __log2f(W)) * kLn2;
+}
+
+hipError_t launch_merge(const float* o_part, const float* lse_part, void* o_dec, float* lse_dec, int S, int B,
+                        int Hq, int Ld, int head_dim, bool bf16, hipStream_t s) {
+  const size_t threads = (size_t)B * Hq * Ld * (head_dim / 4);
+  const dim3 grid((unsigned)((threads + 255) / 256));
+  if (bf16)
+    hipLaunchKernelGGL(merge_kernel<true>, grid, dim3(256), 0, s, o_part, lse_part, o_dec, lse_dec, S, B, Hq, Ld, head_dim);
+  else
+    hipLaunchKernelGGL(merge_kernel<false>, grid, dim3(256), 0, s, o_part, lse_part, o_dec, lse_dec, S, B, Hq, Ld, head_dim);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Chunk cache copy [B][N][1+C][H][d] -> [B][N][H][1+C][d], 16 bytes per thread.
+__global__ __launch_bounds__(256) void cache_copy_kernel(const u32x4* k_pre, const u32x4* v_pre, u32x4* k_cache,
+                                                          u32x4* v_cache, size_t total, int C1, int Hkv, int cpr) {
+  const size_t gid = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (gid >= total) return;
+  // source order: ((bn*C1 + s)*Hkv + g)*cpr + c
+  const int c = gid % cpr;
+  size_t r = gid / cpr;
+  const int g = r % Hkv;
+  r /= Hkv;
+  const int s = r % C1;
+  const size_t bn = r / C1;
+  const size_t dst = ((bn * Hkv + g) * C1 + s) * cpr + c;
+  k_cache[dst] = k_pre[gid];
+  v_cache[dst] = v_pre[gid];
+}
+
+hipError_t launch_cache_copy(const void* k_pre, const void* v_pre, void* k_cache, void* v_cache, int B, int N, int C,
+                             int Hkv, int head_dim, int elem_bytes, hipStream_t s) {
+  const int cpr = head_dim * elem_bytes / 16;
+  const size_t total = (size_t)B * N * (C + 1) * Hkv * cpr;
+  const dim3 grid((unsigned)((total + 255) / 256));
+  hipLaunchKernelGGL(cache_copy_kernel, grid, dim3(256), 0, s, (const u32x4*)k_pre, (const u32x4*)v_pre,
+                     (u32x4*)k_cache, (u32x4*)v_cache, total, C + 1, Hkv, cpr);
+  return hipGetLastError();
+}
+
+}  // namespace pd

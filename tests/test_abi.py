@@ -1,0 +1,139 @@
+"""C-ABI boundary tests that run without a GPU.
+
+The library must load, export every symbol include/pd.h declares, and reject
+bad arguments on the host before anything is launched (so these calls never
+reach the HIP runtime).  Pointers here are fake, aligned or misaligned
+integers: validation only inspects them.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_10537_amd import _lib
+from paper_2606_10537_amd._lib import PD_BF16, PD_FP32, Dims, PdError
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+A = 1 << 20          # a fake, 16-byte aligned address
+MIS = A + 8          # misaligned
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return _lib.load()
+
+
+def header_symbols():
+    with open(os.path.join(ROOT, "include", "pd.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(pd_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    syms = header_symbols()
+    assert set(syms) == set(_lib.EXPORTS)
+    for s in syms:
+        assert hasattr(lib, s), s
+
+
+def test_version_and_status_strings(lib):
+    assert b"gfx950" in lib.pd_version()
+    for code, name in _lib.STATUS.items():
+        assert lib.pd_status_string(code).decode() == name
+
+
+def dims(**kw):
+    base = dict(batch=1, n_chunks=4, chunk_len=128, q_len=16, m_len=32, dec_len=32, n_heads_q=4,
+                n_heads_kv=4, head_dim=64, dtype=PD_BF16)
+    base.update(kw)
+    return Dims(**base)
+
+
+def prefill(d, ws=A, wsn=1 << 30, **ptrs):
+    names = ["q_pre", "k_pre", "v_pre", "q_qm", "k_qm", "v_qm", "o", "k_cache", "v_cache", "tok_score", "key_mean"]
+    args = [ptrs.get(n, A) for n in names]
+    lib = _lib.load()
+    dd = d.c() if d is not None else None
+    return lib.pd_prefill_chunks(ctypes.byref(dd) if dd is not None else None, *args, ws, wsn, None)
+
+
+def test_prefill_validation(lib):
+    assert prefill(None) == 1
+    assert prefill(dims(batch=0)) == 2
+    assert prefill(dims(n_chunks=1025)) == 2
+    assert prefill(dims(chunk_len=0)) == 2
+    assert prefill(dims(chunk_len=5000)) == 2
+    assert prefill(dims(q_len=0)) == 2
+    assert prefill(dims(m_len=-1)) == 2
+    assert prefill(dims(qm_per_chunk=2)) == 2
+    assert prefill(dims(n_heads_q=6, n_heads_kv=4)) == 3
+    assert prefill(dims(head_dim=96)) == 3
+    assert prefill(dims(dtype=7)) == 3
+    assert prefill(dims(), q_pre=None) == 1
+    assert b"q_pre" in lib.pd_last_error_message()
+    assert prefill(dims(), key_mean=None) == 1
+    assert prefill(dims(), o=MIS) == 4
+    assert prefill(dims(), ws=None) == 5
+    assert prefill(dims(), wsn=16) == 5
+    assert prefill(dims(), ws=MIS) == 4
+
+
+def test_select_validation(lib):
+    d = dims()
+    c = ctypes.byref(d.c())
+    ws = _lib.pd_workspace_bytes(d, 2, 64, 0, 1)
+    assert ws > 0
+    call = lambda k, bt, q=A, cs=None, w=A, wn=ws: lib.pd_score_select(c, k, bt, q, A, A, A, A, cs, w, wn, None)
+    assert call(0, 64) == 2
+    assert call(5, 64) == 2          # top_k > N
+    assert call(2, 0) == 2
+    assert call(2, 129) == 2         # tok_budget > C
+    assert call(2, 64, q=None) == 1
+    assert call(2, 64, cs=MIS) == 4
+    assert call(2, 64, wn=ws - 1) == 5
+
+
+def test_decode_validation(lib):
+    d = dims(dtype=PD_BF16)
+    c = ctypes.byref(d.c())
+
+    def call(k=2, bt=64, n_static=16, splits=1, ks=A, o=A, w=A, wn=1 << 30, lse=None):
+        return lib.pd_sparse_decode_attn(c, k, bt, A, A, A, A, A, A, A, ks, ks, n_static, o, lse, splits, w, wn, None)
+
+    assert call(k=0) == 2
+    assert call(k=5) == 2
+    assert call(bt=200) == 2
+    assert call(n_static=49) == 2     # > q_len + m_len
+    assert call(n_static=-1) == 2
+    assert call(splits=65) == 2
+    assert call(ks=None) == 1         # static rows requested but not given
+    assert call(o=None) == 1
+    assert call(lse=MIS) == 4
+    need = _lib.pd_workspace_bytes(d, 2, 64, 4, 2)
+    assert need > 0
+    assert call(splits=4, wn=need - 1) == 5
+    assert call(splits=4, w=None) == 5
+
+
+def test_size_queries():
+    d = dims(batch=2, n_chunks=3, chunk_len=100, n_heads_kv=2, n_heads_q=4, head_dim=128, dtype=PD_BF16)
+    assert _lib.pd_cache_bytes(d) == 2 * 3 * 2 * 101 * 128 * 2
+    d32 = dims(dtype=PD_FP32)
+    assert _lib.pd_cache_bytes(d32) == 1 * 4 * 4 * 129 * 64 * 4
+    assert _lib.pd_workspace_bytes(dims(batch=0), 0, 0, 0, 0) == 0
+    assert _lib.pd_workspace_bytes(d, 0, 0, 0, 0) >= 2 * 3 * 4 * (100 + 16) * 4
+    # One shard needs no decode workspace; S shards need S partial outputs.
+    assert _lib.pd_workspace_bytes(d, 2, 50, 1, 2) == 0
+    assert _lib.pd_workspace_bytes(d, 2, 50, 3, 2) >= 3 * 2 * 4 * 32 * 129 * 4
+    # The automatic shard count never exceeds the KV tile count.
+    for k, bt in [(1, 1), (2, 50), (3, 100)]:
+        s = _lib.pd_decode_splits(d, k, bt, 0, 0)
+        assert 1 <= s <= max(1, -(-(k * (1 + bt) + 32) // 64))
+
+
+def test_binding_raises_on_error():
+    with pytest.raises(PdError) as ei:
+        _lib._check(2)
+    assert ei.value.status == 2

@@ -1,0 +1,260 @@
+"""GPU parity: every C-ABI entry point against the fp64 oracle on the same inputs.
+
+Tolerances (from the method's acceptance rules): outputs max-abs <= 1e-2 for
+bf16 inputs and <= 1e-5 for fp32 inputs; the chunk cache bit-exact; key means
+within relative 1e-5; token scores within 1e-4 absolute; chunk and token index
+sets by rule A (exact wherever the oracle's score gap exceeds 1e-3); decode
+outputs checked with the oracle run on the GPU's own indices.
+"""
+
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_path import (check_topk_rule_a, h64, random_decode_inputs, random_indices, random_prefill_inputs,
+                      run_decode, run_prefill, run_select)
+from paper_2606_10537_amd._lib import PD_BF16, PD_FP32, Dims
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+TOL = {PD_BF16: 1e-2, PD_FP32: 1e-5}
+
+
+def bits(t):
+    """Raw element bits of a host tensor (bf16 -> int16, fp32 -> int32)."""
+    t = t.detach().cpu()
+    return t.view(torch.int16 if t.dtype == torch.bfloat16 else torch.int32).numpy()
+
+
+def prefill_units_check(d, x, out, units, check_e=True):
+    """Oracle check of the listed (b, n) units: O for every head, cache bits, key mean, e."""
+    tol = TOL[d.dtype]
+    for (b, n) in units:
+        xs = {k: h64(v[b:b + 1, n:n + 1] if (k.endswith("_pre") or d.qm_per_chunk) else v[b:b + 1])
+              for k, v in x.items()}
+        e = np.zeros(d.chunk_len)
+        for h in range(d.n_heads_q):
+            u = oracle.prefill_unit_ref(xs["q_pre"], xs["k_pre"], xs["v_pre"], xs["q_qm"], xs["k_qm"], xs["v_qm"],
+                                        0, 0, h, d.q_len, d.sm_scale)
+            got = h64(out["o"][b, n, :, h])
+            err = np.abs(got - u["o"]).max()
+            assert err <= tol, f"prefill O (b={b}, n={n}, h={h}) max-abs {err}"
+            e += u["e_head"]
+        assert np.array_equal(bits(out["k_cache"][b, n]), oracle.cache_ref(bits(x["k_pre"][b:b + 1, n:n + 1]))[0, 0])
+        assert np.array_equal(bits(out["v_cache"][b, n]), oracle.cache_ref(bits(x["v_pre"][b:b + 1, n:n + 1]))[0, 0])
+        km = oracle.key_mean_ref(xs["k_pre"])[0, 0]
+        np.testing.assert_allclose(h64(out["key_mean"][b, n]), km, rtol=1e-5, atol=1e-6 * np.abs(km).max())
+        if check_e:
+            np.testing.assert_allclose(h64(out["tok_score"][b, n]), e, rtol=0, atol=1e-4)
+
+
+# --------------------------------------------------------------------------- stage (a)
+
+PREFILL_CASES = [
+    # dtype, B, N, C, Lq, Lm, Hq, Hkv, D, per_chunk
+    (PD_BF16, 2, 3, 128, 16, 32, 4, 4, 64, 0),
+    (PD_BF16, 1, 2, 100, 17, 5, 4, 2, 128, 0),
+    (PD_BF16, 2, 2, 200, 40, 0, 6, 1, 128, 1),
+    (PD_BF16, 1, 3, 64, 64, 63, 2, 2, 64, 0),
+    (PD_BF16, 1, 1, 1, 1, 0, 1, 1, 128, 0),
+    (PD_FP32, 1, 4, 128, 16, 32, 4, 4, 64, 0),
+    (PD_FP32, 2, 2, 77, 9, 3, 4, 2, 128, 1),
+    (PD_FP32, 1, 1, 1, 1, 0, 1, 1, 64, 0),
+]
+
+
+@pytest.mark.parametrize("case", PREFILL_CASES, ids=[str(c) for c in PREFILL_CASES])
+def test_prefill_parity(case):
+    dt, B, N, C, Lq, Lm, Hq, Hkv, D, pc = case
+    d = Dims(B, N, C, Lq, Lm, 8, Hq, Hkv, D, dt, 0.0, pc)
+    x = random_prefill_inputs(d, seed=hash(case) % 10000, scale=1.0 if dt == PD_BF16 else 0.125)
+    out = run_prefill(d, x)
+    torch.cuda.synchronize()
+    prefill_units_check(d, x, out, [(b, n) for b in range(B) for n in range(N)])
+
+
+def test_prefill_golden_fp32():
+    """The hand-derived worked example, zero-padded from d = 2 to d = 64 (dot products unchanged)."""
+    g = json.load(open(os.path.join(GOLDEN, "prefill_worked_example.json")))
+    d = Dims(1, 1, 2, 1, 1, 1, 1, 1, 64, PD_FP32, 1.0, 0)
+    x = {}
+    for k in ("q_pre", "k_pre", "v_pre", "q_qm", "k_qm", "v_qm"):
+        a = np.array(g[k], dtype=np.float32)
+        pad = np.zeros(a.shape[:-1] + (64,), np.float32)
+        pad[..., :2] = a
+        x[k] = torch.from_numpy(pad).cuda()
+    out = run_prefill(d, x)
+    torch.cuda.synchronize()
+    from fractions import Fraction
+    want = np.array([[float(Fraction(v)) for v in row] for row in g["expect_o_rows"]])
+    np.testing.assert_allclose(h64(out["o"][0, 0, :, 0, :2]), want, atol=1e-6)
+    assert np.all(h64(out["o"][0, 0, :, 0, 2:]) == 0)
+    np.testing.assert_allclose(h64(out["tok_score"][0, 0]), [float(Fraction(v)) for v in g["expect_tok_score"]],
+                               atol=1e-6)
+    np.testing.assert_allclose(h64(out["key_mean"][0, 0, 0, :2]), g["expect_key_mean"], atol=1e-7)
+
+
+def test_prefill_deterministic():
+    d = Dims(1, 3, 300, 20, 10, 8, 4, 2, 128, PD_BF16)
+    x = random_prefill_inputs(d, seed=5)
+    a = run_prefill(d, x)
+    b = run_prefill(d, x)
+    torch.cuda.synchronize()
+    for k in a:
+        assert np.array_equal(bits(a[k]), bits(b[k])), k
+
+
+# --------------------------------------------------------------------------- stage (b)
+
+def test_select_golden():
+    g = json.load(open(os.path.join(GOLDEN, "select_worked_example.json")))
+    q = np.zeros((1, 2, 2, 64), np.float32)
+    q[..., :2] = np.array(g["q_dec"], np.float32)
+    km = np.zeros((1, 3, 1, 64), np.float32)
+    km[..., :2] = np.array(g["key_mean"], np.float32)
+    ts = torch.tensor(g["tok_score"], dtype=torch.float32).cuda()
+    for case in g["cases"]:
+        d = Dims(1, 3, 4, 1, 0, 2, 2, 1, 64, PD_FP32, 1.0, 0)
+        ci, tsl, cs = run_select(d, case["top_k"], case["tok_budget"], torch.from_numpy(q).cuda(),
+                                 torch.from_numpy(km).cuda(), ts)
+        torch.cuda.synchronize()
+        assert ci.cpu().tolist() == [case["chunk_idx"]]
+        assert tsl.cpu().tolist() == [case["tok_slot"]]
+        np.testing.assert_allclose(h64(cs)[0], g["expect_scores"], atol=1e-6)
+
+
+SELECT_CASES = [
+    # dtype, B, N, C, Ld, Hq, Hkv, D, K, Bt
+    (PD_BF16, 2, 8, 1024, 64, 8, 8, 128, 2, 512),
+    (PD_BF16, 1, 16, 1024, 32, 7, 1, 128, 4, 256),
+    (PD_BF16, 3, 5, 100, 17, 4, 2, 64, 5, 100),     # K = N, Bt = C
+    (PD_BF16, 1, 1, 33, 3, 2, 2, 64, 1, 1),
+    (PD_FP32, 2, 40, 300, 9, 4, 4, 64, 7, 33),
+    (PD_FP32, 1, 1024, 16, 4, 2, 1, 64, 10, 16),
+]
+
+
+@pytest.mark.parametrize("case", SELECT_CASES, ids=[str(c) for c in SELECT_CASES])
+def test_select_parity(case):
+    dt, B, N, C, Ld, Hq, Hkv, D, K, Bt = case
+    d = Dims(B, N, C, 4, 0, Ld, Hq, Hkv, D, dt)
+    g = torch.Generator().manual_seed(hash(case) % 10000)
+    tdt = torch.bfloat16 if dt == PD_BF16 else torch.float32
+    q = (torch.randn((B, Ld, Hq, D), generator=g) + 0.3 * torch.randn((1, 1, Hq, D), generator=g)).to(tdt).cuda()
+    km = torch.randn((B, N, Hkv, D), generator=g).cuda()
+    ts = torch.rand((B, N, C), generator=g).cuda() * 5
+    ci, tsl, cs = run_select(d, K, Bt, q, km, ts)
+    torch.cuda.synchronize()
+    s_ref = oracle.chunk_scores_ref(h64(q), h64(km))
+    np.testing.assert_allclose(h64(cs), s_ref, rtol=1e-5, atol=1e-5)
+    e = h64(ts)
+    for b in range(B):
+        check_topk_rule_a(s_ref[b], ci[b].cpu().numpy(), K)
+        for kk, n in enumerate(ci[b].cpu().tolist()):
+            got = tsl[b, kk].cpu().numpy() - 1
+            check_topk_rule_a(e[b, n], got, Bt)
+            if Bt == C:
+                assert got.tolist() == list(range(C))
+
+
+def test_select_ties_and_zero_query():
+    """Q_dec = 0 gives all-zero scores: the first K chunks; equal token scores: the first Bt slots."""
+    d = Dims(2, 9, 50, 4, 0, 8, 4, 2, 64, PD_BF16)
+    q = torch.zeros((2, 8, 4, 64), dtype=torch.bfloat16).cuda()
+    km = torch.randn((2, 9, 2, 64)).cuda()
+    ts = torch.ones((2, 9, 50)).cuda()
+    ci, tsl, cs = run_select(d, 3, 7, q, km, ts)
+    torch.cuda.synchronize()
+    assert ci.cpu().tolist() == [[0, 1, 2]] * 2
+    assert tsl.cpu().tolist() == [[list(range(1, 8))] * 3] * 2
+
+
+# --------------------------------------------------------------------------- stage (c)
+
+def decode_check(d, K, Bt, dec, cache, ci, ts, k_static, v_static, n_static, o, lse, heads=None, batches=None):
+    tol = TOL[d.dtype]
+    cih, tsh = ci.cpu().numpy(), ts.cpu().numpy()
+    for b in (batches if batches is not None else range(d.batch)):
+        # Only the selected chunks of sequence b reach the oracle (same rows, re-indexed).
+        sel = cih[b].tolist()
+        kc = h64(cache["k_cache"][b:b + 1, sel])
+        vc = h64(cache["v_cache"][b:b + 1, sel])
+        ks = h64(k_static[b:b + 1]) if n_static else np.zeros((1, 0, d.n_heads_kv, d.head_dim))
+        vs = h64(v_static[b:b + 1]) if n_static else np.zeros((1, 0, d.n_heads_kv, d.head_dim))
+        dq, dk, dv = (h64(dec[n][b:b + 1]) for n in ("q_dec", "k_dec", "v_dec"))
+        ci0 = np.arange(K, dtype=np.int32)[None]
+        for h in (heads if heads is not None else range(d.n_heads_q)):
+            ro, rl = oracle.decode_unit_ref(dq, dk, dv, kc, vc, ci0, tsh[b:b + 1], ks, vs, n_static, 0, h,
+                                            d.sm_scale)
+            err = np.abs(h64(o[b, :, h]) - ro).max()
+            assert err <= tol, f"decode O (b={b}, h={h}) max-abs {err}"
+            if lse is not None:
+                np.testing.assert_allclose(h64(lse[b, h]), rl, rtol=1e-5, atol=1e-4)
+
+
+DECODE_CASES = [
+    # dtype, B, N, C, Lq, Lm, Ld, Hq, Hkv, D, K, Bt, n_static, splits
+    (PD_BF16, 2, 4, 128, 16, 32, 32, 4, 4, 64, 2, 100, 16, 1),
+    (PD_BF16, 1, 6, 200, 20, 0, 70, 4, 2, 128, 3, 150, 20, 3),
+    (PD_BF16, 2, 5, 64, 8, 8, 1, 7, 1, 128, 5, 64, 0, 0),
+    (PD_BF16, 1, 3, 300, 30, 2, 130, 8, 8, 128, 2, 77, 32, 0),
+    (PD_BF16, 1, 3, 300, 30, 2, 130, 8, 8, 128, 2, 77, 32, 7),
+    (PD_FP32, 1, 4, 128, 16, 32, 32, 4, 4, 64, 2, 128, 16, 1),
+    (PD_FP32, 2, 3, 90, 5, 5, 40, 4, 2, 128, 2, 30, 10, 4),
+    (PD_FP32, 1, 2, 16, 4, 0, 1, 2, 1, 64, 1, 1, 0, 0),
+]
+
+
+@pytest.mark.parametrize("case", DECODE_CASES, ids=[str(c) for c in DECODE_CASES])
+def test_decode_parity(case):
+    dt, B, N, C, Lq, Lm, Ld, Hq, Hkv, D, K, Bt, ns, S = case
+    d = Dims(B, N, C, Lq, Lm, Ld, Hq, Hkv, D, dt)
+    sc = 1.0 if dt == PD_BF16 else 0.125
+    x = random_prefill_inputs(d, seed=hash(case) % 1000, scale=sc)
+    cache = run_prefill(d, x)
+    dec = random_decode_inputs(d, seed=hash(case) % 1000 + 1, scale=sc)
+    ci, ts = random_indices(d, K, Bt, seed=3)
+    o, lse = run_decode(d, K, Bt, dec, cache, ci, ts, x["k_qm"], x["v_qm"], ns, num_splits=S)
+    torch.cuda.synchronize()
+    decode_check(d, K, Bt, dec, cache, ci, ts, x["k_qm"], x["v_qm"], ns, o, lse)
+
+
+@pytest.mark.parametrize("dt", [PD_BF16, PD_FP32])
+def test_decode_dense_equivalence(dt):
+    """K = N and every slot kept: the sparse decode equals dense attention over all prefix rows."""
+    d = Dims(1, 3, 64, 8, 8, 16, 4, 2, 64, dt)
+    sc = 1.0 if dt == PD_BF16 else 0.125
+    x = random_prefill_inputs(d, seed=11, scale=sc)
+    cache = run_prefill(d, x)
+    dec = random_decode_inputs(d, seed=12, scale=sc)
+    ci = torch.arange(3, dtype=torch.int32).cuda()[None]
+    ts = torch.arange(1, 65, dtype=torch.int32).cuda().repeat(1, 3, 1)
+    o, _ = run_decode(d, 3, 64, dec, cache, ci, ts, x["k_qm"], x["v_qm"], 8)
+    torch.cuda.synchronize()
+    scale = 1 / np.sqrt(64)
+    for h in range(4):
+        g = h // 2
+        k = np.concatenate([h64(cache["k_cache"][0, :, g]).reshape(-1, 64), h64(x["k_qm"][0, :8, g]), h64(dec["k_dec"][0, :, g])])
+        v = np.concatenate([h64(cache["v_cache"][0, :, g]).reshape(-1, 64), h64(x["v_qm"][0, :8, g]), h64(dec["v_dec"][0, :, g])])
+        q = h64(dec["q_dec"][0, :, h])
+        s = scale * q @ k.T
+        p = np.exp(s - s.max(1, keepdims=True))
+        ref = (p / p.sum(1, keepdims=True)) @ v
+        assert np.abs(h64(o[0, :, h]) - ref).max() <= TOL[dt]
+
+
+def test_decode_split_invariance():
+    """Any shard count gives the same output within rounding (LSE merge of the shards)."""
+    d = Dims(1, 4, 256, 16, 0, 64, 4, 4, 128, PD_BF16)
+    x = random_prefill_inputs(d, seed=21)
+    cache = run_prefill(d, x)
+    dec = random_decode_inputs(d, seed=22)
+    ci, ts = random_indices(d, 4, 200, seed=23)
+    outs = [run_decode(d, 4, 200, dec, cache, ci, ts, x["k_qm"], x["v_qm"], 16, num_splits=s)[0] for s in (1, 2, 5, 13)]
+    torch.cuda.synchronize()
+    for o in outs[1:]:
+        assert (o.float() - outs[0].float()).abs().max().item() <= 1e-2
