@@ -1,0 +1,250 @@
+"""Benchmark of the block-sparse attention path on one MI355X.
+
+One step = one pass of the whole hot path over one batch of synthetic input:
+prefill of every layer (chunk prefill + cache write + token/chunk summaries),
+then T denoising steps, each running, for every layer, chunk scoring / top-K /
+top-B selection and the sparse decode attention.
+
+Prints one JSON line.  `value` = denoising steps per second of the whole job
+(T / time of one step, prefill included); the prefill MFMA rate and the decode
+attention HBM rate are reported next to it.  Inputs are resident in HBM before
+the timed region starts.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA (published)
+PEAK_HBM_GBPS = 8000.0         # MI355X HBM3E (published)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=3)
+    p.add_argument("--warmup", type=int, default=1)
+    p.add_argument("--workload", type=int, default=5, help="workload id (1-5)")
+    p.add_argument("--layers", type=int, default=0, help="override the layer count (0 = workload's)")
+    p.add_argument("--pool", type=int, default=2, help="distinct prefill input sets cycled over layers")
+    p.add_argument("--dec-pool", type=int, default=4, help="decode input slots per layer")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU time budget of the oracle sample")
+    return p.parse_args()
+
+
+def algorithmic(w, layers):
+    """Algorithmic FLOPs / bytes per launch of the prefill and decode attention kernels."""
+    B, N, C, Lq, Lm, Ld = w.batch, w.n_chunks, w.chunk_len, w.q_len, w.m_len, w.dec_len
+    Hq, Hkv, d, K, Bt = w.n_heads_q, w.n_heads_kv, w.head_dim, w.top_k, w.tok_budget
+    eb = 2
+    Sc = 1 + C + Lq + Lm
+    L_kv = K * (1 + Bt) + Lq + Ld
+    pre_flop = 4.0 * Sc * Sc * d * Hq * B * N
+    # Reads Q, K, V of every chunk sequence once, writes O and the cache once.
+    pre_bytes = eb * d * B * (N * (1 + C) * (Hq + 2 * Hkv) + (Lq + Lm) * (Hq + 2 * Hkv)
+                              + N * Sc * Hq + 2 * N * (1 + C) * Hkv)
+    dec_flop = 4.0 * Ld * L_kv * d * Hq * B
+    # Gathered + static + own K and V rows per (b, kv head), Q read and O write per (b, q head).
+    dec_bytes = eb * d * B * (2 * L_kv * Hkv + 2 * Ld * Hq)
+    return pre_flop, pre_bytes, dec_flop, dec_bytes
+
+
+def cpu_baseline(w, budget_s):
+    """Time the fp64 oracle on a bounded sample of the same workload, extrapolated to one step."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import oracle
+    from paper_2606_10537_amd import synth
+
+    rng = np.random.default_rng(0)
+    B, N, C, Lq, Lm, Ld = w.batch, w.n_chunks, w.chunk_len, w.q_len, w.m_len, w.dec_len
+    Hq, Hkv, d, K, Bt = w.n_heads_q, w.n_heads_kv, w.head_dim, w.top_k, w.tok_budget
+    L, T = w.layers, w.steps
+    # One sequence, one chunk of the workload's shapes (values from the synthetic generator).
+    w1 = synth.Workload(**{**w.__dict__, "batch": 1, "n_chunks": 1})
+    x = {k: v.double().numpy() for k, v in synth.make_prefill(w1, 0, "cpu").items()}
+    dec = {k: v.double().numpy() for k, v in synth.make_decode(w1, 0, 0, "cpu").items()}
+
+    def timed(fn, share):
+        n, t0 = 0, time.perf_counter()
+        while True:
+            fn()
+            n += 1
+            el = time.perf_counter() - t0
+            if el >= share * budget_s:
+                return el / n, n
+
+    t_pre, n_pre = timed(lambda: oracle.prefill_unit_ref(x["q_pre"], x["k_pre"], x["v_pre"], x["q_qm"], x["k_qm"],
+                                                         x["v_qm"], 0, 0, 0, Lq), 0.5)
+    km = rng.standard_normal((1, N, Hkv, d))
+    ts = rng.standard_normal((1, N, C))
+    qd = rng.standard_normal((1, Ld, Hq, d))
+    t_sel, n_sel = timed(lambda: oracle.score_select_ref(qd, km, ts, K, Bt), 0.15)
+    kc = rng.standard_normal((1, K, Hkv, 1 + C, d))
+    vc = rng.standard_normal((1, K, Hkv, 1 + C, d))
+    ci = np.arange(K, dtype=np.int32)[None]
+    tsl = np.sort(rng.permuted(np.tile(np.arange(1, C + 1), (1, K, 1)), axis=2)[:, :, :Bt], axis=2).astype(np.int32)
+    t_dec, n_dec = timed(lambda: oracle.decode_unit_ref(dec["q_dec"], dec["k_dec"], dec["v_dec"], kc, vc, ci, tsl,
+                                                        x["k_qm"], x["v_qm"], Lq, 0, 0), 0.35)
+    step_s = t_pre * B * N * Hq * L + t_sel * B * T * L + t_dec * B * Hq * T * L
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {
+        "value": T / step_s, "unit": "denoising steps/s", "cores": threads, "kind": "oracle",
+        "sample": (f"fp64 oracle: {n_pre} prefill units (1 chunk x 1 head, S_c={1 + C + Lq + Lm}), "
+                   f"{n_sel} score/select calls (1 sequence), {n_dec} decode units (1 sequence x 1 head, "
+                   f"L_kv={K * (1 + Bt) + Lq + Ld}); per-unit times x unit counts of one step "
+                   f"({B * N * Hq * L} prefill, {B * T * L} select, {B * Hq * T * L} decode units); extrapolated"),
+        "seconds_per_step_extrapolated": step_s,
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (got --gpus {args.gpus}); the path shards by "
+              "sequence with no communication, so multi-GPU figures are not produced.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2606_10537_amd import _lib, synth
+
+    lib = _lib.load()
+    w = synth.WORKLOADS[args.workload]
+    if args.layers:
+        w = synth.Workload(**{**w.__dict__, "layers": args.layers})
+    d = w.dims()
+    dev = "cuda"
+    dt = w.torch_dtype
+    B, N, C, Hq, Hkv, D = w.batch, w.n_chunks, w.chunk_len, w.n_heads_q, w.n_heads_kv, w.head_dim
+    L, T, K, Bt, Ld = w.layers, w.steps, w.top_k, w.tok_budget, w.dec_len
+    n_static = w.q_len
+
+    # ---- resident inputs and buffers -------------------------------------------------
+    pool = [synth.make_prefill(w, layer=i, device=dev) for i in range(min(args.pool, L))]
+    dec_slots = max(1, args.dec_pool)
+    dec_pool = [[synth.make_decode(w, layer=l, step=s, device=dev) for s in range(dec_slots)] for l in range(L)]
+    o_pre = torch.empty((B, N, d.seq_len, Hq, D), dtype=dt, device=dev)
+    k_cache = [torch.empty((B, N, Hkv, C + 1, D), dtype=dt, device=dev) for _ in range(L)]
+    v_cache = [torch.empty((B, N, Hkv, C + 1, D), dtype=dt, device=dev) for _ in range(L)]
+    tok_score = [torch.empty((B, N, C), dtype=torch.float32, device=dev) for _ in range(L)]
+    key_mean = [torch.empty((B, N, Hkv, D), dtype=torch.float32, device=dev) for _ in range(L)]
+    ws_pre = torch.empty(_lib.pd_workspace_bytes(d, which=0), dtype=torch.uint8, device=dev)
+    ws_sel = torch.empty(_lib.pd_workspace_bytes(d, K, Bt, 0, 1), dtype=torch.uint8, device=dev)
+    ws_dec = torch.empty(max(16, _lib.pd_workspace_bytes(d, K, Bt, 0, 2)), dtype=torch.uint8, device=dev)
+    chunk_idx = torch.empty((B, K), dtype=torch.int32, device=dev)
+    tok_slot = torch.empty((B, K, Bt), dtype=torch.int32, device=dev)
+    o_dec = torch.empty((B, Ld, Hq, D), dtype=dt, device=dev)
+    splits = _lib.pd_decode_splits(d, K, Bt, n_static, 0)
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+
+    n_ev = L * T
+    ev_pre = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(L)]
+    ev_dec = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_ev)]
+    ev_mid = torch.cuda.Event(enable_timing=True)
+
+    def one_step(record):
+        for l in range(L):
+            x = pool[l % len(pool)]
+            if record:
+                ev_pre[l][0].record(stream)
+            _lib.pd_prefill_chunks(d, x["q_pre"], x["k_pre"], x["v_pre"], x["q_qm"], x["k_qm"], x["v_qm"], o_pre,
+                                   k_cache[l], v_cache[l], tok_score[l], key_mean[l], ws_pre, sh)
+            if record:
+                ev_pre[l][1].record(stream)
+        if record:
+            ev_mid.record(stream)
+        i = 0
+        for t in range(T):
+            for l in range(L):
+                dd = dec_pool[l][t % dec_slots]
+                _lib.pd_score_select(d, K, Bt, dd["q_dec"], key_mean[l], tok_score[l], chunk_idx, tok_slot, None,
+                                     ws_sel, sh)
+                if record:
+                    ev_dec[i][0].record(stream)
+                _lib.pd_sparse_decode_attn(d, K, Bt, dd["q_dec"], dd["k_dec"], dd["v_dec"], k_cache[l], v_cache[l],
+                                           chunk_idx, tok_slot, pool[l % len(pool)]["k_qm"],
+                                           pool[l % len(pool)]["v_qm"], n_static, o_dec, None, 0, ws_dec, sh)
+                if record:
+                    ev_dec[i][1].record(stream)
+                i += 1
+
+    for _ in range(args.warmup):
+        one_step(False)
+    torch.cuda.synchronize()
+
+    pre_ms, dec_ms, dec_kernel_ms, step_ms = [], [], [], []
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    for s in range(args.steps):
+        start.record(stream)
+        one_step(True)
+        end.record(stream)
+        torch.cuda.synchronize()
+        step_ms.append(start.elapsed_time(end))
+        pre_ms.append(start.elapsed_time(ev_mid))
+        dec_ms.append(ev_mid.elapsed_time(end))
+        dec_kernel_ms.extend(a.elapsed_time(b) for a, b in ev_dec)
+        print(f"[bench] step {s}: {step_ms[-1]:.1f} ms (prefill {pre_ms[-1]:.1f} ms, decode loop {dec_ms[-1]:.1f} ms)",
+              file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+
+    ms = sum(step_ms) / len(step_ms)
+    pre_flop, pre_bytes, dec_flop, dec_bytes = algorithmic(w, L)
+    pre_ms_layer = sum(pre_ms) / len(pre_ms) / L
+    dec_kern_ms = sum(dec_kernel_ms) / len(dec_kernel_ms)
+    dec_tflops = dec_flop / (dec_kern_ms * 1e-3) / 1e12
+    dec_gbps = dec_bytes / (dec_kern_ms * 1e-3) / 1e9
+    pre_tflops = pre_flop / (pre_ms_layer * 1e-3) / 1e12
+    ridge = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBPS * 1e9)
+    dec_bound = "mfma" if dec_flop / dec_bytes > ridge else "hbm"
+    if dec_bound == "mfma":
+        roof = {"bound": "mfma", "achieved": round(dec_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(dec_tflops / PEAK_BF16_TFLOPS, 4)}
+    else:
+        roof = {"bound": "hbm", "achieved": round(dec_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                "frac": round(dec_gbps / PEAK_HBM_GBPS, 4)}
+    roof.update({"kernel": "decode_bf16_kernel<128> (pd_sparse_decode_attn, one launch per layer and step)",
+                 "traffic": None, "launch_ms": round(dec_kern_ms, 5), "flop_per_launch": dec_flop,
+                 "bytes_per_launch": dec_bytes})
+
+    res = {
+        "metric": "denoising steps/sec + decode-attn HBM GB/s + prefill MFMA TFLOP/s at 32K",
+        "value": round(T / (ms * 1e-3), 3),
+        "unit": "denoising steps/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{w.context // 1024}K context ({w.name}): B={B}, layers={L}, N={N}, C={C}, "
+                               f"L_q={w.q_len}, L_m={w.m_len}, L_d={Ld}, H_q/H_kv={Hq}/{Hkv}, d={D}, K={K}, "
+                               f"B_tok={Bt}, T={T}",
+                   "global_batch": B, "seq_len": w.context, "parallelism": "single GPU",
+                   "decode_splits": splits},
+        "decode_steps_per_s": round(T / (sum(dec_ms) / len(dec_ms) * 1e-3), 3),
+        "decode_attn_hbm_gbps": round(dec_gbps, 1),
+        "decode_attn_hbm_frac": round(dec_gbps / PEAK_HBM_GBPS, 4),
+        "decode_attn_tflops": round(dec_tflops, 2),
+        "prefill_ms_per_layer": round(pre_ms_layer, 3),
+        "prefill_tflops": round(pre_tflops, 2),
+        "prefill_mfma_frac": round(pre_tflops / PEAK_BF16_TFLOPS, 4),
+        "roofline": roof,
+        "wall_s": round(wall, 3),
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(res))
+
+
+if __name__ == "__main__":
+    main()
