@@ -50,28 +50,47 @@ struct WaveState {
   float qmass;  // this lane's partial mass on the query columns (prefill only)
 };
 
+// Thread -> (row group, 16-byte chunk) mappings used to stage a 64-row tile.
+// K: thread t takes chunk t % CH of rows RPT*(t / CH) .. +RPT-1 (row-major
+// stores, every bank hit equally often).  V: each wave takes all row groups
+// and CH/4 chunks, so that the 8 transposed stores of a thread (V^T rows 8c+e)
+// from one wave land on V^T rows whose 36-dword-strided bases alternate bank
+// halves: every bank is hit exactly twice per store instruction.
+template <int D>
+struct StageMap {
+  int rgk, ck, rgv, cv;
+  __device__ StageMap(int tid) {
+    using T = Tile<D>;
+    const int lane = tid & 63, wave = tid >> 6, cpw = T::CH / 4;
+    ck = tid % T::CH;
+    rgk = tid / T::CH;
+    rgv = lane / cpw;
+    cv = wave * cpw + lane % cpw;
+  }
+};
+
 // Stage one K/V tile held in registers into LDS.
 template <int D>
-__device__ __forceinline__ void stage_tile(uint16_t* Ks, uint16_t* Vt, int rg, int c,
+__device__ __forceinline__ void stage_tile(uint16_t* Ks, uint16_t* Vt, const StageMap<D>& mp,
                                            const u32x4 (&kr)[Tile<D>::RPT],
                                            const u32x4 (&vr)[Tile<D>::RPT]) {
   using T = Tile<D>;
 #pragma unroll
-  for (int i = 0; i < T::RPT; ++i) st16(Ks + (rg * T::RPT + i) * T::KPAD + 8 * c, kr[i]);
-  const int col = vt_col(rg * T::RPT);
+  for (int i = 0; i < T::RPT; ++i) st16(Ks + (mp.rgk * T::RPT + i) * T::KPAD + 8 * mp.ck, kr[i]);
+  const int col = vt_col(mp.rgv * T::RPT);
+  // Element e of each of the RPT rows, packed two halves per v_perm_b32:
+  // selector 0x05040100 takes the low halves of (lo, hi), 0x07060302 the high.
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    const int w = e >> 1, sh = (e & 1) * 16;
-    uint32_t h0 = (vr[0][w] >> sh) & 0xffffu;
-    uint32_t h1 = (vr[1][w] >> sh) & 0xffffu;
-    uint16_t* dst = Vt + (8 * c + e) * T::VPAD + col;
+    const int w = e >> 1;
+    const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
+    uint16_t* dst = Vt + (8 * mp.cv + e) * T::VPAD + col;
+    const uint32_t a = __builtin_amdgcn_perm(vr[1][w], vr[0][w], sel);
     if constexpr (T::RPT == 4) {
-      uint32_t h2 = (vr[2][w] >> sh) & 0xffffu;
-      uint32_t h3 = (vr[3][w] >> sh) & 0xffffu;
-      u32x2 v = {h0 | (h1 << 16), h2 | (h3 << 16)};
-      *reinterpret_cast<u32x2*>(dst) = v;
+      const uint32_t b = __builtin_amdgcn_perm(vr[3][w], vr[2][w], sel);
+      *reinterpret_cast<u32x2*>(dst) = u32x2{a, b};
     } else {
-      *reinterpret_cast<uint32_t*>(dst) = h0 | (h1 << 16);
+      *reinterpret_cast<uint32_t*>(dst) = a;
     }
   }
 }
@@ -95,27 +114,24 @@ __device__ __forceinline__ void tile_step(WaveState<D>& st, const uint16_t* Ks, 
       s[kb] = mfma32x32x16(a, st.qf[ks], s[kb]);
     }
   }
-  // Key of s[kb][r]: 32*kb + 8*(r/4) + 4*grp + r%4.
-  float mx = -INFINITY;
-  if (kv_valid >= 64) {
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        s[kb][r] *= scale_log2;
-        mx = fmaxf(mx, s[kb][r]);
-      }
-  } else {
+  // Key of s[kb][r]: 32*kb + 8*(r/4) + 4*grp + r%4.  The max is taken on raw
+  // scores (the scale is positive) and the scale is folded into one FMA:
+  // p = exp2(s * scale_log2 - m).
+  if (kv_valid < 64) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int key = 32 * kb + 8 * (r >> 2) + 4 * grp + (r & 3);
-        s[kb][r] = key < kv_valid ? s[kb][r] * scale_log2 : -INFINITY;
-        mx = fmaxf(mx, s[kb][r]);
+        s[kb][r] = key < kv_valid ? s[kb][r] : -INFINITY;
       }
   }
-  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  float mx = -INFINITY;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; r += 2) mx = fmaxf(mx, fmaxf(s[kb][r], s[kb][r + 1]));
+  mx = fmaxf(mx, __shfl_xor(mx, 32)) * scale_log2;
   const bool upd = mx > st.m + 8.0f;
   if (__ballot(upd)) {
     const float mnew = upd ? mx : st.m;
@@ -128,18 +144,25 @@ __device__ __forceinline__ void tile_step(WaveState<D>& st, const uint16_t* Ks, 
 #pragma unroll
       for (int r = 0; r < 16; ++r) st.o[db][r] *= alpha;
   }
-  bf16x8 pf[4];
+  const float nm = -st.m;
+  uint32_t pk[16];
   float lsum = 0.f;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const float pv = fast_exp2(s[kb][r] - st.m);
-      s[kb][r] = pv;
-      lsum += pv;
-      pf[2 * kb + (r >> 3)][r & 7] = (__bf16)pv;
+    for (int r = 0; r < 16; r += 2) {
+      const float p0 = fast_exp2(fmaf(s[kb][r], scale_log2, nm));
+      const float p1 = fast_exp2(fmaf(s[kb][r + 1], scale_log2, nm));
+      s[kb][r] = p0;
+      s[kb][r + 1] = p1;
+      lsum += p0 + p1;
+      pk[8 * kb + r / 2] = __builtin_bit_cast(uint32_t, bf16x2{(__bf16)p0, (__bf16)p1});
     }
   st.l += lsum;
+  bf16x8 pf[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk)
+    pf[kk] = __builtin_bit_cast(bf16x8, u32x4{pk[4 * kk], pk[4 * kk + 1], pk[4 * kk + 2], pk[4 * kk + 3]});
   if (qlo < qhi) {
     float qs = 0.f;
 #pragma unroll
@@ -196,16 +219,44 @@ __device__ __forceinline__ void store_row_f32(float* dst, const WaveState<D>& st
     }
 }
 
+// Double-buffered sweep over KV tiles [t_begin, t_end): tile t is computed from
+// LDS buffer (t - t_begin) & 1 while tile t+1 is staged into the other buffer
+// and tile t+2 is already loading into registers; one barrier per tile.
+// load(t, kr, vr) fills the registers, hook(t, kr, vr) sees them before staging
+// (the prefill writes its cache share there), step(t, Ks, Vt) computes.
+template <int D, class Load, class Hook, class Step>
+__device__ __forceinline__ void kv_sweep(uint16_t* Ks0, uint16_t* Vt0, int t_begin, int t_end, const StageMap<D>& mp,
+                                         Load&& load, Hook&& hook, Step&& step) {
+  using T = Tile<D>;
+  constexpr int KSZ = T::BN * T::KPAD, VSZ = D * T::VPAD;
+  u32x4 kr[T::RPT], vr[T::RPT];
+  load(t_begin, kr, vr);
+  hook(t_begin, kr, vr);
+  stage_tile<D>(Ks0, Vt0, mp, kr, vr);
+  if (t_begin + 1 < t_end) load(t_begin + 1, kr, vr);
+  __syncthreads();
+  for (int t = t_begin; t < t_end; ++t) {
+    const int cur = (t - t_begin) & 1;
+    step(t, Ks0 + cur * KSZ, Vt0 + cur * VSZ);
+    if (t + 1 < t_end) {
+      hook(t + 1, kr, vr);
+      stage_tile<D>(Ks0 + (cur ^ 1) * KSZ, Vt0 + (cur ^ 1) * VSZ, mp, kr, vr);
+      if (t + 2 < t_end) load(t + 2, kr, vr);
+    }
+    __syncthreads();
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Stage (a): chunk prefill.  Workgroup = (b, n, h, 128-row query tile).
 // Also writes the chunk KV cache (each KV tile by exactly one workgroup of the
 // (b, n, kv-head) group), the per-head query-column mass of the content rows
 // and the log2-domain LSE of the query rows.
 template <int D>
-__global__ __launch_bounds__(256) void prefill_bf16_kernel(PrefillArgs p) {
+__global__ __launch_bounds__(256, 2) void prefill_bf16_kernel(PrefillArgs p) {
   using T = Tile<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[T::BN * T::KPAD];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[D * T::VPAD];
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2 * T::BN * T::KPAD];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[2 * D * T::VPAD];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, grp = lane >> 5;
@@ -235,60 +286,62 @@ __global__ __launch_bounds__(256) void prefill_bf16_kernel(PrefillArgs p) {
   }
   wave_init(st);
 
-  const int c = tid % T::CH, rg = tid / T::CH;
-  u32x4 kr[T::RPT], vr[T::RPT];
-  auto load = [&](int t) {
+  const StageMap<D> mp(tid);
+  // Row r of the chunk sequence lives at base + r*HD (HD = H_kv*d elements), with
+  // base the chunk's rows for r <= C and the shared query/pseudo-label rows after.
+  // Rows past the end are clamped to the last row: their keys are masked out of
+  // the softmax and their (finite) values get probability 0.
+  const int HD = p.Hkv * D;
+  const uint16_t* k_lo = p.k_pre + (chunk * C1 * p.Hkv + g) * D;
+  const uint16_t* v_lo = p.v_pre + (chunk * C1 * p.Hkv + g) * D;
+  const uint16_t* k_hi = p.k_qm + (qm_base * p.Hkv + g) * D - (size_t)C1 * HD;
+  const uint16_t* v_hi = p.v_qm + (qm_base * p.Hkv + g) * D - (size_t)C1 * HD;
+  const int offk = mp.rgk * T::RPT * HD + 8 * mp.ck;   // this thread's first K row, within a tile
+  const int offv = mp.rgv * T::RPT * HD + 8 * mp.cv;
+  auto load = [&](int t, u32x4 (&kr)[T::RPT], u32x4 (&vr)[T::RPT]) {
+    const int r0 = t * T::BN;
+    if (r0 + T::BN <= C1 || (r0 >= C1 && r0 + T::BN <= p.Sc)) {
+      // Whole tile inside one source: rows r0.. at base + r0*HD, no per-row selects.
+      const uint16_t* kb = (r0 < C1 ? k_lo : k_hi) + (size_t)r0 * HD;
+      const uint16_t* vb = (r0 < C1 ? v_lo : v_hi) + (size_t)r0 * HD;
 #pragma unroll
-    for (int i = 0; i < T::RPT; ++i) {
-      const int row = t * T::BN + rg * T::RPT + i;
-      if (row < C1) {
-        const size_t off = ((chunk * C1 + row) * p.Hkv + g) * D + 8 * c;
-        kr[i] = ld16(p.k_pre + off);
-        vr[i] = ld16(p.v_pre + off);
-      } else if (row < p.Sc) {
-        const size_t off = ((qm_base + (row - C1)) * p.Hkv + g) * D + 8 * c;
-        kr[i] = ld16(p.k_qm + off);
-        vr[i] = ld16(p.v_qm + off);
-      } else {
-        kr[i] = u32x4{0, 0, 0, 0};
-        vr[i] = u32x4{0, 0, 0, 0};
+      for (int i = 0; i < T::RPT; ++i) {
+        kr[i] = ld16(kb + (unsigned)(offk + i * HD));
+        vr[i] = ld16(vb + (unsigned)(offv + i * HD));
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < T::RPT; ++i) {
+        const int rk = min(r0 + mp.rgk * T::RPT + i, p.Sc - 1);
+        const int rv = min(r0 + mp.rgv * T::RPT + i, p.Sc - 1);
+        kr[i] = ld16((rk < C1 ? k_lo : k_hi) + (unsigned)(rk * HD + 8 * mp.ck));
+        vr[i] = ld16((rv < C1 ? v_lo : v_hi) + (unsigned)(rv * HD + 8 * mp.cv));
       }
     }
   };
-  auto cache_write = [&](int t) {
+  // Each KV tile of the (b, n, kv head) group is written to the cache by exactly
+  // one workgroup of that group: query tile t % n_qt of head g*G + (t / n_qt) % G.
+  auto cache_write = [&](int t, const u32x4 (&kr)[T::RPT], const u32x4 (&vr)[T::RPT]) {
     const bool writer = (t % p.n_qt == qt) && ((t / p.n_qt) % p.G == h % p.G);
     if (!writer) return;
+    const size_t base = (chunk * p.Hkv + g) * C1;
 #pragma unroll
     for (int i = 0; i < T::RPT; ++i) {
-      const int row = t * T::BN + rg * T::RPT + i;
-      if (row < C1) {
-        const size_t off = (((chunk * p.Hkv + g) * C1) + row) * D + 8 * c;
-        st16(p.k_cache + off, kr[i]);
-        st16(p.v_cache + off, vr[i]);
-      }
+      const int rk = t * T::BN + mp.rgk * T::RPT + i;
+      if (rk < C1) st16(p.k_cache + (base + rk) * D + 8 * mp.ck, kr[i]);
+      const int rv = t * T::BN + mp.rgv * T::RPT + i;
+      if (rv < C1) st16(p.v_cache + (base + rv) * D + 8 * mp.cv, vr[i]);
     }
   };
 
   const int qc_lo = C1, qc_hi = C1 + p.Lq;   // query columns counted by Eq. 5
-  load(0);
-  cache_write(0);
-  stage_tile<D>(Ks, Vt, rg, c, kr, vr);
-  __syncthreads();
-  for (int t = 0; t < p.n_kvt; ++t) {
-    if (t + 1 < p.n_kvt) load(t + 1);
-    if (wave_active) {
-      const int t0 = t * T::BN;
-      const int kv_valid = min(T::BN, p.Sc - t0);
-      const int lo = max(qc_lo - t0, 0), hi = min(qc_hi - t0, T::BN);
-      tile_step<D>(st, Ks, Vt, l32, grp, p.scale_log2, kv_valid, lo, hi);
-    }
-    __syncthreads();
-    if (t + 1 < p.n_kvt) {
-      cache_write(t + 1);
-      stage_tile<D>(Ks, Vt, rg, c, kr, vr);
-    }
-    __syncthreads();
-  }
+  kv_sweep<D>(Ks, Vt, 0, p.n_kvt, mp, load, cache_write, [&](int t, const uint16_t* ks, const uint16_t* vt) {
+    if (!wave_active) return;
+    const int t0 = t * T::BN;
+    const int kv_valid = min(T::BN, p.Sc - t0);
+    const int lo = max(qc_lo - t0, 0), hi = min(qc_hi - t0, T::BN);
+    tile_step<D>(st, ks, vt, l32, grp, p.scale_log2, kv_valid, lo, hi);
+  });
   if (!wave_active) return;
 
   const float ltot = st.l + __shfl_xor(st.l, 32);
@@ -311,10 +364,11 @@ __global__ __launch_bounds__(256) void prefill_bf16_kernel(PrefillArgs p) {
 // is head g*G + rho / L_d, decode row rho % L_d.  KV row j of the shard walks:
 // [kept chunks: BOS + kept slots] ; [static rows] ; [own rows].
 template <int D>
-__global__ __launch_bounds__(256) void decode_bf16_kernel(DecodeArgs p) {
+__global__ __launch_bounds__(256, 2) void decode_bf16_kernel(DecodeArgs p) {
   using T = Tile<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[T::BN * T::KPAD];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[D * T::VPAD];
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2 * T::BN * T::KPAD];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[2 * D * T::VPAD];
+  __shared__ __attribute__((aligned(16))) int rowtab[kDecodeTableRows];   // cache row (n*Hkv*(C+1) + slot) of gathered rows
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, grp = lane >> 5;
@@ -348,56 +402,79 @@ __global__ __launch_bounds__(256) void decode_bf16_kernel(DecodeArgs p) {
   const int t_begin = (int)(((long long)n_kvt * sp) / p.S);
   const int t_end = (int)(((long long)n_kvt * (sp + 1)) / p.S);
 
-  const int c = tid % T::CH, rg = tid / T::CH;
-  const size_t cache_bg = ((size_t)b * p.N * p.Hkv + g) * C1;   // + (n*Hkv)*C1 + slot
-  const int32_t* cidx = p.chunk_idx + (size_t)b * p.K;
-  const int32_t* tslot = p.tok_slot + (size_t)b * p.K * p.Bt;
-  u32x4 kr[T::RPT], vr[T::RPT];
-  auto load = [&](int t) {
+  const StageMap<D> mp(tid);
+  const size_t cache_bg = ((size_t)b * p.N * p.Hkv + g) * C1;   // + n*Hkv*C1 + slot
+  // Gathered rows of this shard: row codes into LDS once (the host keeps every
+  // shard within kDecodeTableRows rows), so tile loads need no index fetch.
+  const int j_lo = t_begin * T::BN;
+  const int j_hi = min(t_end * T::BN, n_sel);
+  {
+    const int32_t* cidx = p.chunk_idx + (size_t)b * p.K;
+    const int32_t* tslot = p.tok_slot + (size_t)b * p.K * p.Bt;
+    for (int j = j_lo + tid; j < j_hi; j += T::NT) {
+      const int kk = j / (1 + p.Bt), s = j - kk * (1 + p.Bt);
+      const int slot = s == 0 ? 0 : tslot[kk * p.Bt + s - 1];
+      rowtab[j - j_lo] = cidx[kk] * p.Hkv * C1 + slot;
+    }
+  }
+  __syncthreads();
+  // Row j of the shard: gathered cache rows (offset from the LDS table), then
+  // static rows, then own rows, each at base + row*HD for the latter two.  Rows
+  // past L_kv are clamped to the last row (masked out of the softmax).
+  const int HD = p.Hkv * D;
+  const uint16_t* kc = p.k_cache + cache_bg * D;
+  const uint16_t* vc = p.v_cache + cache_bg * D;
+  const size_t sb = ((size_t)b * p.Ls * p.Hkv + g) * D - (size_t)n_sel * HD;
+  const size_t db = ((size_t)b * p.Ld * p.Hkv + g) * D - (size_t)(n_sel + p.n_static) * HD;
+  const uint16_t* ks_ = p.k_static ? p.k_static + sb : p.k_dec + db;
+  const uint16_t* vs_ = p.v_static ? p.v_static + sb : p.v_dec + db;
+  const uint16_t* kd_ = p.k_dec + db;
+  const uint16_t* vd_ = p.v_dec + db;
+  const int tab_hi = max(j_hi - j_lo - 1, 0);
+  auto row_ptr = [&](int j, const uint16_t* c_, const uint16_t* s_, const uint16_t* d_, int ch) {
+    j = min(j, L_kv - 1);
+    const unsigned tab = (unsigned)rowtab[min(max(j - j_lo, 0), tab_hi)] * D;
+    const uint16_t* base = j < n_sel ? c_ : (j < n_sel + p.n_static ? s_ : d_);
+    const unsigned off = j < n_sel ? tab : (unsigned)(j * HD);
+    return base + off + 8 * ch;
+  };
+  static_assert(T::RPT == 4 || T::RPT == 2, "");
+  auto load = [&](int t, u32x4 (&kr)[T::RPT], u32x4 (&vr)[T::RPT]) {
+    const int r0 = t * T::BN;
+    if (r0 + T::BN <= n_sel) {
+      // Whole tile gathered from the cache: the RPT row codes of a thread are
+      // consecutive table entries (one LDS read).
+      const int* tk = rowtab + (r0 - j_lo) + mp.rgk * T::RPT;
+      const int* tv = rowtab + (r0 - j_lo) + mp.rgv * T::RPT;
+      int ck[T::RPT], cv[T::RPT];
+      if constexpr (T::RPT == 4) {
+        const u32x4 a = *reinterpret_cast<const u32x4*>(tk), b = *reinterpret_cast<const u32x4*>(tv);
 #pragma unroll
-    for (int i = 0; i < T::RPT; ++i) {
-      const int j = t * T::BN + rg * T::RPT + i;
-      const uint16_t *ks = nullptr, *vs = nullptr;
-      size_t off = 0;
-      if (j < n_sel) {
-        const int kk = j / (1 + p.Bt), s = j - kk * (1 + p.Bt);
-        const int nn = cidx[kk];
-        const int slot = s == 0 ? 0 : tslot[kk * p.Bt + s - 1];
-        off = (cache_bg + (size_t)nn * p.Hkv * C1 + slot) * D;
-        ks = p.k_cache;
-        vs = p.v_cache;
-      } else if (j < n_sel + p.n_static) {
-        off = (((size_t)b * p.Ls + (j - n_sel)) * p.Hkv + g) * D;
-        ks = p.k_static;
-        vs = p.v_static;
-      } else if (j < L_kv) {
-        off = (((size_t)b * p.Ld + (j - n_sel - p.n_static)) * p.Hkv + g) * D;
-        ks = p.k_dec;
-        vs = p.v_dec;
-      }
-      if (ks) {
-        kr[i] = ld16(ks + off + 8 * c);
-        vr[i] = ld16(vs + off + 8 * c);
+        for (int i = 0; i < 4; ++i) { ck[i] = (int)a[i]; cv[i] = (int)b[i]; }
       } else {
-        kr[i] = u32x4{0, 0, 0, 0};
-        vr[i] = u32x4{0, 0, 0, 0};
+        const u32x2 a = *reinterpret_cast<const u32x2*>(tk), b = *reinterpret_cast<const u32x2*>(tv);
+#pragma unroll
+        for (int i = 0; i < 2; ++i) { ck[i] = (int)a[i]; cv[i] = (int)b[i]; }
+      }
+#pragma unroll
+      for (int i = 0; i < T::RPT; ++i) {
+        kr[i] = ld16(kc + ((unsigned)ck[i] * D + 8 * mp.ck));
+        vr[i] = ld16(vc + ((unsigned)cv[i] * D + 8 * mp.cv));
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < T::RPT; ++i) {
+        kr[i] = ld16(row_ptr(r0 + mp.rgk * T::RPT + i, kc, ks_, kd_, mp.ck));
+        vr[i] = ld16(row_ptr(r0 + mp.rgv * T::RPT + i, vc, vs_, vd_, mp.cv));
       }
     }
   };
-
-  load(t_begin);
-  stage_tile<D>(Ks, Vt, rg, c, kr, vr);
-  __syncthreads();
-  for (int t = t_begin; t < t_end; ++t) {
-    if (t + 1 < t_end) load(t + 1);
-    if (wave_active) {
-      const int kv_valid = min(T::BN, L_kv - t * T::BN);
-      tile_step<D>(st, Ks, Vt, l32, grp, p.scale_log2, kv_valid, 0, 0);
-    }
-    __syncthreads();
-    if (t + 1 < t_end) stage_tile<D>(Ks, Vt, rg, c, kr, vr);
-    __syncthreads();
-  }
+  auto no_hook = [](int, const u32x4 (&)[T::RPT], const u32x4 (&)[T::RPT]) {};
+  kv_sweep<D>(Ks, Vt, t_begin, t_end, mp, load, no_hook, [&](int t, const uint16_t* ks, const uint16_t* vt) {
+    if (!wave_active) return;
+    const int kv_valid = min(T::BN, L_kv - t * T::BN);
+    tile_step<D>(st, ks, vt, l32, grp, p.scale_log2, kv_valid, 0, 0);
+  });
   if (!wave_active || rho >= GL) return;
 
   const float ltot = st.l + __shfl_xor(st.l, 32);

@@ -62,10 +62,17 @@ pd_status check_dims(const pd_dims* d) {
   if (d->dtype != PD_BF16 && d->dtype != PD_FP32)
     return fail(PD_ERR_UNSUPPORTED, "dtype=%d is neither PD_BF16 nor PD_FP32", d->dtype);
   if (!(std::isfinite(d->sm_scale))) return fail(PD_ERR_BAD_DIMS, "sm_scale is not finite");
+  // Grid sizes must fit one launch dimension.
   const long long sc = 1LL + d->chunk_len + d->q_len + d->m_len;
   if (sc > (1LL << 24) || d->dec_len > (1 << 24))
     return fail(PD_ERR_BAD_DIMS, "sequence length too large");
-  // Grid sizes must fit one launch dimension.
+  // Kernels address rows inside one sequence's cache, chunk sequence or decode
+  // block with 32-bit element offsets.
+  if ((long long)d->n_chunks * d->n_heads_kv * (d->chunk_len + 1) * d->head_dim >= (1LL << 31))
+    return fail(PD_ERR_BAD_DIMS, "one sequence's cache (n_chunks*n_heads_kv*(chunk_len+1)*head_dim) must stay below 2^31 elements");
+  if (sc * std::max(d->n_heads_q, d->n_heads_kv) * d->head_dim >= (1LL << 31) ||
+      (long long)d->dec_len * d->n_heads_q * d->head_dim >= (1LL << 31))
+    return fail(PD_ERR_BAD_DIMS, "rows of one sequence exceed 2^31 elements");
   const long long grid = (long long)d->batch * d->n_chunks * d->n_heads_q * cdiv(sc, 64);
   if (grid >= (1LL << 31)) return fail(PD_ERR_BAD_DIMS, "problem too large for one launch");
   return PD_OK;
@@ -109,12 +116,24 @@ int decode_units(const pd_dims* d) {
 
 // Requested shard count: explicit, or chosen so that the decode grid reaches
 // about two workgroups per CU while every shard keeps >= 4 KV tiles of 64 rows.
+// The bf16 kernel also needs every shard to fit its LDS row table (at most
+// kDecodeTableRows rows, i.e. kDecodeTableRows/64 tiles), whatever n_static is.
+int min_splits(const pd_dims* d, int top_k, int tok_budget) {
+  const long long n_sel = (long long)top_k * (1 + tok_budget);
+  if (d->dtype != PD_BF16 || n_sel <= pd::kDecodeTableRows) return 1;
+  const long long lkv_max = n_sel + d->q_len + d->m_len + d->dec_len;
+  return cdiv(cdiv(lkv_max, 64), pd::kDecodeTableRows / 64);
+}
+
 int requested_splits(const pd_dims* d, int top_k, int tok_budget, int num_splits) {
-  if (num_splits > 0) return num_splits;
-  const long long lkv0 = (long long)top_k * (1 + tok_budget) + d->dec_len;
-  const int max_by_len = std::max(1, cdiv(lkv0, 64) / 4);
-  const int want = cdiv(kTargetWorkgroups, std::max(1, decode_units(d)));
-  return std::max(1, std::min(std::min(want, max_by_len), kMaxSplits));
+  int s = num_splits;
+  if (s <= 0) {
+    const long long lkv0 = (long long)top_k * (1 + tok_budget) + d->dec_len;
+    const int max_by_len = std::max(1, cdiv(lkv0, 64) / 4);
+    const int want = cdiv(kTargetWorkgroups, std::max(1, decode_units(d)));
+    s = std::max(1, std::min(std::min(want, max_by_len), kMaxSplits));
+  }
+  return std::max(s, min_splits(d, top_k, tok_budget));
 }
 
 int effective_splits(const pd_dims* d, int top_k, int tok_budget, int n_static, int num_splits) {

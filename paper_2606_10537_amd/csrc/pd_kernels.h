@@ -5,6 +5,10 @@
 
 namespace pd {
 
+// Gathered KV rows of one decode shard whose cache-row codes fit the kernel's
+// LDS table; the host raises the shard count until every shard fits.
+constexpr int kDecodeTableRows = 2048;
+
 // Stage (a).  Element pointers are bf16 bit patterns (uint16_t) or fp32.
 struct PrefillArgs {
   const uint16_t *q_pre, *k_pre, *v_pre, *q_qm, *k_qm, *v_qm;
