@@ -133,7 +133,8 @@ def main():
     o_pre = torch.empty((B, N, d.seq_len, Hq, D), dtype=dt, device=dev)
     k_cache = [torch.empty((B, N, Hkv, C + 1, D), dtype=dt, device=dev) for _ in range(L)]
     v_cache = [torch.empty((B, N, Hkv, C + 1, D), dtype=dt, device=dev) for _ in range(L)]
-    tok_score = [torch.empty((B, N, C), dtype=torch.float32, device=dev) for _ in range(L)]
+    tok_score = torch.empty((B, N, C), dtype=torch.float32, device=dev)
+    tok_rank = [torch.empty((B, N, C), dtype=torch.int32, device=dev) for _ in range(L)]
     key_mean = [torch.empty((B, N, Hkv, D), dtype=torch.float32, device=dev) for _ in range(L)]
     ws_pre = torch.empty(_lib.pd_workspace_bytes(d, which=0), dtype=torch.uint8, device=dev)
     ws_sel = torch.empty(_lib.pd_workspace_bytes(d, K, Bt, 0, 1), dtype=torch.uint8, device=dev)
@@ -156,7 +157,7 @@ def main():
             if record:
                 ev_pre[l][0].record(stream)
             _lib.pd_prefill_chunks(d, x["q_pre"], x["k_pre"], x["v_pre"], x["q_qm"], x["k_qm"], x["v_qm"], o_pre,
-                                   k_cache[l], v_cache[l], tok_score[l], key_mean[l], ws_pre, sh)
+                                   k_cache[l], v_cache[l], tok_score, tok_rank[l], key_mean[l], ws_pre, sh)
             if record:
                 ev_pre[l][1].record(stream)
         if record:
@@ -165,7 +166,7 @@ def main():
         for t in range(T):
             for l in range(L):
                 dd = dec_pool[l][t % dec_slots]
-                _lib.pd_score_select(d, K, Bt, dd["q_dec"], key_mean[l], tok_score[l], chunk_idx, tok_slot, None,
+                _lib.pd_score_select(d, K, Bt, dd["q_dec"], key_mean[l], tok_rank[l], chunk_idx, tok_slot, None,
                                      ws_sel, sh)
                 if record:
                     ev_dec[i][0].record(stream)

@@ -58,7 +58,7 @@ typedef enum { PD_BF16 = 0, PD_FP32 = 1 } pd_dtype;
 typedef struct {
   int32_t batch;        /* B >= 1                                                   */
   int32_t n_chunks;     /* N, 1..1024                                               */
-  int32_t chunk_len;    /* C, 1..8192 content tokens; the cache holds 1+C rows      */
+  int32_t chunk_len;    /* C, 1..4096 content tokens; the cache holds 1+C rows      */
   int32_t q_len;        /* L_q >= 1 query rows                                      */
   int32_t m_len;        /* L_m >= 0 pseudo-label rows                               */
   int32_t dec_len;      /* L_d >= 1 decode rows                                     */
@@ -70,6 +70,8 @@ typedef struct {
   int32_t qm_per_chunk; /* 0: the q/m rows are one tensor shared by all chunks,
                            [B][L_q+L_m][H][d];  1: one copy per chunk,
                            [B][N][L_q+L_m][H][d]                                    */
+  int32_t out_fp32;     /* 0: o and o_dec have element type dtype; 1: they are fp32
+                           (bf16 inputs, fp32 outputs: no output rounding)          */
 } pd_dims;
 
 /*
@@ -89,11 +91,15 @@ typedef struct {
  *   k_qm, v_qm  likewise with H_kv heads
  * Outputs:
  *   o         [B][N][S_c][H_q][d]   attention output, rows ordered BOS, c, q, m
+ *             (element type dtype, or fp32 when out_fp32 = 1)
  *   k_cache, v_cache [B][N][H_kv][1+C][d]  exact copies of the chunk rows
  *             (BOS at slot 0), chunk-contiguous per KV head
  *   tok_score fp32 [B][N][C]  e(c_j) of Eq. 5: for content token j, the
  *             softmax mass the L_q query rows put on it plus the mass it puts
  *             on the L_q query columns, summed over all H_q heads
+ *   tok_rank  int32 [B][N][C]  rank of token j among the C tokens of its chunk
+ *             by tok_score: 0 = highest, ties to the lower index (Section 5.2:
+ *             tokens are ranked by eviction score)
  *   key_mean  fp32 [B][N][H_kv][d]  mean of the C content keys (BOS excluded)
  * workspace: >= pd_workspace_bytes(dims, 0, 0, 0, 0) bytes.
  * Errors: PD_ERR_BAD_DIMS for a size out of range; see the status list.
@@ -102,19 +108,20 @@ pd_status pd_prefill_chunks(const pd_dims *dims,
                             const void *q_pre, const void *k_pre, const void *v_pre,
                             const void *q_qm, const void *k_qm, const void *v_qm,
                             void *o, void *k_cache, void *v_cache,
-                            float *tok_score, float *key_mean,
+                            float *tok_score, int32_t *tok_rank, float *key_mean,
                             void *workspace, size_t ws_bytes, void *stream);
 
 /*
  * Stage (b), one layer, one denoising step: chunk scores, top-K chunks
  * (Section 5.2, inter-chunk sparsity) and the top-B_tok tokens of each kept
- * chunk by the Eq. 5 score (intra-chunk sparsity).
+ * chunk by the Eq. 5 score (intra-chunk sparsity), read from the token ranks
+ * that pd_prefill_chunks wrote (a token is kept iff its rank < B_tok).
  *
  * The chunk score is an attention-space stand-in for the paper's NLL score:
  *   s[b][n] = sum_h scale * < mean_r q_dec[b][r][h], key_mean[b][n][h/G] >,
  * higher = kept.  Ties rank the lower chunk (token) index first.
  * Inputs:  q_dec [B][L_d][H_q][d] (dims->dtype), key_mean fp32 [B][N][H_kv][d],
- *          tok_score fp32 [B][N][C].
+ *          tok_rank int32 [B][N][C] (a permutation of 0..C-1 per chunk).
  * Outputs: chunk_idx int32 [B][top_k], ascending chunk indices;
  *          tok_slot  int32 [B][top_k][tok_budget], ascending cache slots in
  *          1..C of the kept tokens of chunk chunk_idx[b][k] (slot = token+1);
@@ -123,7 +130,7 @@ pd_status pd_prefill_chunks(const pd_dims *dims,
  * workspace: >= pd_workspace_bytes(dims, top_k, tok_budget, 0, 1) bytes.
  */
 pd_status pd_score_select(const pd_dims *dims, int32_t top_k, int32_t tok_budget,
-                          const void *q_dec, const float *key_mean, const float *tok_score,
+                          const void *q_dec, const float *key_mean, const int32_t *tok_rank,
                           int32_t *chunk_idx, int32_t *tok_slot, float *chunk_score,
                           void *workspace, size_t ws_bytes, void *stream);
 
@@ -139,8 +146,10 @@ pd_status pd_score_select(const pd_dims *dims, int32_t top_k, int32_t tok_budget
  *   [B][L_q+L_m][H_kv][d] (rows 0..n_static-1 used; may be NULL when
  *   n_static = 0); chunk_idx, tok_slot as written by pd_score_select (entries
  *   must lie in 0..N-1 and 1..C).
- * Outputs: o_dec [B][L_d][H_q][d]; lse_dec fp32 [B][H_q][L_d] natural-log
- *   row LSE, or NULL.
+ * Outputs: o_dec [B][L_d][H_q][d] (dtype, or fp32 when out_fp32 = 1);
+ *   lse_dec fp32 [B][H_q][L_d] natural-log
+ *   row LSE, or NULL (bf16 path: the log of the sum of
+ *   the bf16-rounded softmax weights that multiply V, within log(1 + 2^-9)).
  * num_splits: the KV rows are cut into that many shards processed in
  *   parallel and merged by log-sum-exp (the paper's Split-S); 0 = chosen by the
  *   library from the sizes; otherwise 1..64.

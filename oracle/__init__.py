@@ -30,7 +30,7 @@ from .prefill import (
     cache_ref,
     key_mean_ref,
 )
-from .select import chunk_scores_ref, topk_ref, score_select_ref
+from .select import chunk_scores_ref, topk_ref, score_select_ref, token_rank_ref, tokens_by_rank_ref
 from .decode import decode_kv_rows, decode_unit_ref, decode_ref
 
 __all__ = [
@@ -43,6 +43,8 @@ __all__ = [
     "chunk_scores_ref",
     "topk_ref",
     "score_select_ref",
+    "token_rank_ref",
+    "tokens_by_rank_ref",
     "decode_kv_rows",
     "decode_unit_ref",
     "decode_ref",

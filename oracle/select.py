@@ -46,6 +46,32 @@ def topk_ref(x, k):
     return np.sort(order[:k])
 
 
+def token_rank_ref(tok_score):
+    """Rank of every token inside its chunk by Eq. 5 score: 0 = highest, ties to
+    the lower index (Section 5.2: tokens are ranked by eviction score).
+    tok_score (B, N, C) -> int32 (B, N, C)."""
+    e = np.asarray(tok_score, dtype=np.float64)
+    bsz, nch, c = e.shape
+    rank = np.zeros((bsz, nch, c), dtype=np.int32)
+    for b in range(bsz):
+        for n in range(nch):
+            order = np.lexsort((np.arange(c), -e[b, n]))
+            rank[b, n, order] = np.arange(c, dtype=np.int32)
+    return rank
+
+
+def tokens_by_rank_ref(tok_rank, chunk_idx, tok_budget):
+    """Kept slots of each selected chunk: the tokens ranked below tok_budget, as
+    ascending cache slots 1 + j.  Returns int32 (B, K, Btok)."""
+    r = np.asarray(tok_rank)
+    ci = np.asarray(chunk_idx)
+    out = np.zeros(ci.shape + (tok_budget,), dtype=np.int32)
+    for b in range(ci.shape[0]):
+        for kk, n in enumerate(ci[b]):
+            out[b, kk] = 1 + np.nonzero(r[b, n] < tok_budget)[0]
+    return out
+
+
 def score_select_ref(q_dec, key_mean, tok_score, top_k, tok_budget, scale=None):
     """Whole stage (b) for one step.
 

@@ -34,6 +34,7 @@ class PdDims(ctypes.Structure):
         ("q_len", ctypes.c_int32), ("m_len", ctypes.c_int32), ("dec_len", ctypes.c_int32),
         ("n_heads_q", ctypes.c_int32), ("n_heads_kv", ctypes.c_int32), ("head_dim", ctypes.c_int32),
         ("dtype", ctypes.c_int32), ("sm_scale", ctypes.c_float), ("qm_per_chunk", ctypes.c_int32),
+        ("out_fp32", ctypes.c_int32),
     ]
 
 
@@ -52,6 +53,7 @@ class Dims:
     dtype: int = PD_BF16
     sm_scale: float = 0.0
     qm_per_chunk: int = 0
+    out_fp32: int = 0
 
     @property
     def seq_len(self):
@@ -61,7 +63,7 @@ class Dims:
     def c(self):
         return PdDims(self.batch, self.n_chunks, self.chunk_len, self.q_len, self.m_len, self.dec_len,
                       self.n_heads_q, self.n_heads_kv, self.head_dim, self.dtype, self.sm_scale,
-                      self.qm_per_chunk)
+                      self.qm_per_chunk, self.out_fp32)
 
 
 _lib = None
@@ -77,7 +79,7 @@ def load(path: str = LIB_PATH):
     lib = ctypes.CDLL(path)
     vp, sz, i32, fp = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_void_p
     dp = ctypes.POINTER(PdDims)
-    lib.pd_prefill_chunks.argtypes = [dp] + [vp] * 11 + [vp, sz, vp]
+    lib.pd_prefill_chunks.argtypes = [dp] + [vp] * 12 + [vp, sz, vp]
     lib.pd_prefill_chunks.restype = ctypes.c_int
     lib.pd_score_select.argtypes = [dp, i32, i32, vp, fp, fp, vp, vp, fp, vp, sz, vp]
     lib.pd_score_select.restype = ctypes.c_int
@@ -139,19 +141,19 @@ def pd_decode_splits(dims: Dims, top_k, tok_budget, n_static, num_splits=0) -> i
 
 
 def pd_prefill_chunks(dims: Dims, q_pre, k_pre, v_pre, q_qm, k_qm, v_qm, o, k_cache, v_cache,
-                      tok_score, key_mean, workspace, stream=None):
+                      tok_score, tok_rank, key_mean, workspace, stream=None):
     """Stage (a) for one layer (see include/pd.h)."""
     _check(load().pd_prefill_chunks(
         ctypes.byref(dims.c()), _ptr(q_pre), _ptr(k_pre), _ptr(v_pre), _ptr(q_qm), _ptr(k_qm), _ptr(v_qm),
-        _ptr(o), _ptr(k_cache), _ptr(v_cache), _ptr(tok_score), _ptr(key_mean),
+        _ptr(o), _ptr(k_cache), _ptr(v_cache), _ptr(tok_score), _ptr(tok_rank), _ptr(key_mean),
         _ptr(workspace), _nbytes(workspace), _stream(stream)))
 
 
-def pd_score_select(dims: Dims, top_k, tok_budget, q_dec, key_mean, tok_score, chunk_idx, tok_slot,
+def pd_score_select(dims: Dims, top_k, tok_budget, q_dec, key_mean, tok_rank, chunk_idx, tok_slot,
                     chunk_score, workspace, stream=None):
     """Stage (b) for one layer and step (see include/pd.h)."""
     _check(load().pd_score_select(
-        ctypes.byref(dims.c()), top_k, tok_budget, _ptr(q_dec), _ptr(key_mean), _ptr(tok_score),
+        ctypes.byref(dims.c()), top_k, tok_budget, _ptr(q_dec), _ptr(key_mean), _ptr(tok_rank),
         _ptr(chunk_idx), _ptr(tok_slot), _ptr(chunk_score), _ptr(workspace), _nbytes(workspace),
         _stream(stream)))
 

@@ -46,7 +46,8 @@ struct WaveState {
   bf16x8 qf[Tile<D>::KS];
   f32x16 o[Tile<D>::DB];
   float m;      // running row max (log2 domain), shared by lanes l and l^32
-  float l;      // this lane's partial row sum
+  float l;      // this lane's partial sum of the bf16-rounded weights that multiply V
+  float lx;     // this lane's partial sum of the unrounded weights (prefill only)
   float qmass;  // this lane's partial mass on the query columns (prefill only)
 };
 
@@ -98,7 +99,10 @@ __device__ __forceinline__ void stage_tile(uint16_t* Ks, uint16_t* Vt, const Sta
 // One KV tile for one wave: S^T = K Q^T, online softmax, O^T += V^T P^T.
 // kv_valid: number of valid keys in this tile (64 except in a ragged last tile).
 // qlo/qhi: key range (tile-relative) counted into qmass; empty when qlo >= qhi.
-template <int D>
+// EXACT: also keep the unrounded row sum and the query-column mass (prefill).
+// O is normalised by the sum of the same bf16-rounded weights that multiply V,
+// so rounding P perturbs a convex combination instead of scaling O.
+template <int D, bool EXACT>
 __device__ __forceinline__ void tile_step(WaveState<D>& st, const uint16_t* Ks, const uint16_t* Vt,
                                           int l32, int grp, float scale_log2, int kv_valid,
                                           int qlo, int qhi) {
@@ -138,7 +142,10 @@ __device__ __forceinline__ void tile_step(WaveState<D>& st, const uint16_t* Ks, 
     const float alpha = fast_exp2(st.m - mnew);
     st.m = mnew;
     st.l *= alpha;
-    st.qmass *= alpha;
+    if constexpr (EXACT) {
+      st.lx *= alpha;
+      st.qmass *= alpha;
+    }
 #pragma unroll
     for (int db = 0; db < T::DB; ++db)
 #pragma unroll
@@ -155,15 +162,21 @@ __device__ __forceinline__ void tile_step(WaveState<D>& st, const uint16_t* Ks, 
       const float p1 = fast_exp2(fmaf(s[kb][r + 1], scale_log2, nm));
       s[kb][r] = p0;
       s[kb][r + 1] = p1;
-      lsum += p0 + p1;
+      if constexpr (EXACT) lsum += p0 + p1;
       pk[8 * kb + r / 2] = __builtin_bit_cast(uint32_t, bf16x2{(__bf16)p0, (__bf16)p1});
     }
-  st.l += lsum;
+  if constexpr (EXACT) st.lx += lsum;
+  // Sum of the rounded weights: one v_dot2c_f32_bf16 with (1, 1) per packed pair.
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  float lr = st.l;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) lr = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[i]), ones, lr, false);
+  st.l = lr;
   bf16x8 pf[4];
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk)
     pf[kk] = __builtin_bit_cast(bf16x8, u32x4{pk[4 * kk], pk[4 * kk + 1], pk[4 * kk + 2], pk[4 * kk + 3]});
-  if (qlo < qhi) {
+  if (EXACT && qlo < qhi) {
     float qs = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -190,6 +203,7 @@ __device__ __forceinline__ void wave_init(WaveState<D>& st) {
   for (int db = 0; db < Tile<D>::DB; ++db) st.o[db] = f32x16{0};
   st.m = -INFINITY;
   st.l = 0.f;
+  st.lx = 0.f;
   st.qmass = 0.f;
 }
 
@@ -340,20 +354,22 @@ __global__ __launch_bounds__(256, 2) void prefill_bf16_kernel(PrefillArgs p) {
     const int t0 = t * T::BN;
     const int kv_valid = min(T::BN, p.Sc - t0);
     const int lo = max(qc_lo - t0, 0), hi = min(qc_hi - t0, T::BN);
-    tile_step<D>(st, ks, vt, l32, grp, p.scale_log2, kv_valid, lo, hi);
+    tile_step<D, true>(st, ks, vt, l32, grp, p.scale_log2, kv_valid, lo, hi);
   });
   if (!wave_active) return;
 
   const float ltot = st.l + __shfl_xor(st.l, 32);
+  const float lxtot = st.lx + __shfl_xor(st.lx, 32);
   const float qtot = st.qmass + __shfl_xor(st.qmass, 32);
   const float inv = 1.0f / ltot;
   if (qrow < p.Sc) {
-    uint16_t* dst = p.o + ((chunk * p.Sc + qrow) * p.Hq + h) * D;
-    store_row_bf16<D>(dst, st, inv, grp);
+    const size_t orow = ((chunk * p.Sc + qrow) * p.Hq + h) * D;
+    if (p.out_f32) store_row_f32<D>(reinterpret_cast<float*>(p.o) + orow, st, inv, grp);
+    else store_row_bf16<D>(p.o + orow, st, inv, grp);
     if (grp == 0) {
       const size_t hb = chunk * p.Hq + h;
-      if (qrow >= 1 && qrow < C1) p.part_i[hb * p.C + (qrow - 1)] = qtot * inv;
-      if (qrow >= qc_lo && qrow < qc_hi) p.lse_q[hb * p.Lq + (qrow - qc_lo)] = st.m + __log2f(ltot);
+      if (qrow >= 1 && qrow < C1) p.part_i[hb * p.C + (qrow - 1)] = qtot / lxtot;
+      if (qrow >= qc_lo && qrow < qc_hi) p.lse_q[hb * p.Lq + (qrow - qc_lo)] = st.m + __log2f(lxtot);
     }
   }
 }
@@ -473,7 +489,7 @@ __global__ __launch_bounds__(256, 2) void decode_bf16_kernel(DecodeArgs p) {
   kv_sweep<D>(Ks, Vt, t_begin, t_end, mp, load, no_hook, [&](int t, const uint16_t* ks, const uint16_t* vt) {
     if (!wave_active) return;
     const int kv_valid = min(T::BN, L_kv - t * T::BN);
-    tile_step<D>(st, ks, vt, l32, grp, p.scale_log2, kv_valid, 0, 0);
+    tile_step<D, false>(st, ks, vt, l32, grp, p.scale_log2, kv_valid, 0, 0);
   });
   if (!wave_active || rho >= GL) return;
 
@@ -481,8 +497,9 @@ __global__ __launch_bounds__(256, 2) void decode_bf16_kernel(DecodeArgs p) {
   const float inv = 1.0f / ltot;
   const float lse2 = st.m + __log2f(ltot);
   if (p.S == 1) {
-    uint16_t* dst = reinterpret_cast<uint16_t*>(p.o_dec) + (((size_t)b * p.Ld + rr) * p.Hq + hq) * D;
-    store_row_bf16<D>(dst, st, inv, grp);
+    const size_t orow = (((size_t)b * p.Ld + rr) * p.Hq + hq) * D;
+    if (p.out_f32) store_row_f32<D>(reinterpret_cast<float*>(p.o_dec) + orow, st, inv, grp);
+    else store_row_bf16<D>(reinterpret_cast<uint16_t*>(p.o_dec) + orow, st, inv, grp);
     if (p.lse_dec && grp == 0) p.lse_dec[((size_t)b * p.Hq + hq) * p.Ld + rr] = lse2 * kLn2;
   } else {
     const size_t row = (((size_t)sp * p.B + b) * p.Hq + hq) * p.Ld + rr;

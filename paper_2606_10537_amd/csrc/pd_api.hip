@@ -55,6 +55,8 @@ pd_status check_dims(const pd_dims* d) {
     return fail(PD_ERR_BAD_DIMS, "head counts %d/%d must be >= 1", d->n_heads_q, d->n_heads_kv);
   if (d->qm_per_chunk != 0 && d->qm_per_chunk != 1)
     return fail(PD_ERR_BAD_DIMS, "qm_per_chunk=%d must be 0 or 1", d->qm_per_chunk);
+  if (d->out_fp32 != 0 && d->out_fp32 != 1)
+    return fail(PD_ERR_BAD_DIMS, "out_fp32=%d must be 0 or 1", d->out_fp32);
   if (d->n_heads_q % d->n_heads_kv != 0)
     return fail(PD_ERR_UNSUPPORTED, "n_heads_q=%d is not a multiple of n_heads_kv=%d", d->n_heads_q, d->n_heads_kv);
   if (d->head_dim != 64 && d->head_dim != 128)
@@ -94,15 +96,9 @@ PrefillWs prefill_ws(const pd_dims* d) {
   return w;
 }
 
-struct SelectWs {
-  size_t qbar, scores, total;
-};
-SelectWs select_ws(const pd_dims* d) {
-  SelectWs w;
-  w.qbar = 0;
-  w.scores = round_up((size_t)d->batch * d->n_heads_q * d->head_dim * sizeof(float));
-  w.total = w.scores + round_up((size_t)d->batch * d->n_chunks * sizeof(float));
-  return w;
+// Chunk-score terms [B][N][H_q * row splits].
+size_t select_ws(const pd_dims* d) {
+  return round_up((size_t)d->batch * d->n_chunks * d->n_heads_q * pd::select_row_splits(d->dec_len) * sizeof(float));
 }
 
 int decode_qtiles(const pd_dims* d) {
@@ -203,7 +199,7 @@ size_t pd_workspace_bytes(const pd_dims* d, int32_t top_k, int32_t tok_budget, i
   if (check_dims(d) != PD_OK) return 0;
   switch (which) {
     case 0: return prefill_ws(d).total;
-    case 1: return select_ws(d).total;
+    case 1: return select_ws(d);
     case 2:
       if (top_k < 1 || tok_budget < 1 || num_splits < 0 || num_splits > kMaxSplits) return 0;
       return decode_ws_bytes(d, requested_splits(d, top_k, tok_budget, num_splits));
@@ -218,8 +214,8 @@ int32_t pd_decode_splits(const pd_dims* d, int32_t top_k, int32_t tok_budget, in
 
 pd_status pd_prefill_chunks(const pd_dims* d, const void* q_pre, const void* k_pre, const void* v_pre,
                             const void* q_qm, const void* k_qm, const void* v_qm, void* o, void* k_cache,
-                            void* v_cache, float* tok_score, float* key_mean, void* workspace, size_t ws_bytes,
-                            void* stream) {
+                            void* v_cache, float* tok_score, int32_t* tok_rank, float* key_mean, void* workspace,
+                            size_t ws_bytes, void* stream) {
   PD_RETURN_IF(check_dims(d));
   PD_REQUIRE_PTR(q_pre);
   PD_REQUIRE_PTR(k_pre);
@@ -231,6 +227,7 @@ pd_status pd_prefill_chunks(const pd_dims* d, const void* q_pre, const void* k_p
   PD_REQUIRE_PTR(k_cache);
   PD_REQUIRE_PTR(v_cache);
   PD_REQUIRE_PTR(tok_score);
+  PD_REQUIRE_PTR(tok_rank);
   PD_REQUIRE_PTR(key_mean);
   const PrefillWs w = prefill_ws(d);
   PD_RETURN_IF(check_ws(workspace, ws_bytes, w.total));
@@ -260,6 +257,7 @@ pd_status pd_prefill_chunks(const pd_dims* d, const void* q_pre, const void* k_p
   a.G = a.Hq / a.Hkv;
   a.Sc = 1 + a.C + a.Lq + a.Lm;
   a.qm_per_chunk = d->qm_per_chunk;
+  a.out_f32 = d->out_fp32;
   a.scale_log2 = scale_of(d) * 1.4426950408889634f;
   a.n_qt = cdiv(a.Sc, bf16 ? 128 : 64);
   a.n_kvt = cdiv(a.Sc, 64);
@@ -298,12 +296,14 @@ pd_status pd_prefill_chunks(const pd_dims* d, const void* q_pre, const void* k_p
     err = pd::launch_escore_f32(e, d->head_dim, s);
     if (err != hipSuccess) return hip_status(err, "token-score kernel");
   }
+  err = pd::launch_token_rank(tok_score, tok_rank, a.B, a.N, a.C, s);
+  if (err != hipSuccess) return hip_status(err, "token-rank kernel");
   err = pd::launch_key_mean(k_cache, key_mean, a.B, a.N, a.C, a.Hkv, d->head_dim, bf16, s);
   return hip_status(err, "key-mean kernel");
 }
 
 pd_status pd_score_select(const pd_dims* d, int32_t top_k, int32_t tok_budget, const void* q_dec,
-                          const float* key_mean, const float* tok_score, int32_t* chunk_idx, int32_t* tok_slot,
+                          const float* key_mean, const int32_t* tok_rank, int32_t* chunk_idx, int32_t* tok_slot,
                           float* chunk_score, void* workspace, size_t ws_bytes, void* stream) {
   PD_RETURN_IF(check_dims(d));
   if (top_k < 1 || top_k > d->n_chunks)
@@ -312,20 +312,18 @@ pd_status pd_score_select(const pd_dims* d, int32_t top_k, int32_t tok_budget, c
     return fail(PD_ERR_BAD_DIMS, "tok_budget=%d must be in 1..chunk_len=%d", tok_budget, d->chunk_len);
   PD_REQUIRE_PTR(q_dec);
   PD_REQUIRE_PTR(key_mean);
-  PD_REQUIRE_PTR(tok_score);
+  PD_REQUIRE_PTR(tok_rank);
   PD_REQUIRE_PTR(chunk_idx);
   PD_REQUIRE_PTR(tok_slot);
   if (chunk_score && !aligned16(chunk_score))
     return fail(PD_ERR_MISALIGNED, "pointer 'chunk_score' is not 16-byte aligned");
-  const SelectWs w = select_ws(d);
-  PD_RETURN_IF(check_ws(workspace, ws_bytes, w.total));
-  char* ws = (char*)workspace;
+  PD_RETURN_IF(check_ws(workspace, ws_bytes, select_ws(d)));
   pd::SelectArgs a{};
   a.q_dec = q_dec;
   a.key_mean = key_mean;
-  a.tok_score = tok_score;
-  a.qbar = (float*)(ws + w.qbar);
-  a.scores = chunk_score ? chunk_score : (float*)(ws + w.scores);
+  a.tok_rank = tok_rank;
+  a.partial = (float*)workspace;
+  a.chunk_score = chunk_score;
   a.chunk_idx = chunk_idx;
   a.tok_slot = tok_slot;
   a.B = d->batch;
@@ -338,6 +336,7 @@ pd_status pd_score_select(const pd_dims* d, int32_t top_k, int32_t tok_budget, c
   a.D = d->head_dim;
   a.K = top_k;
   a.Bt = tok_budget;
+  a.NS = pd::select_row_splits(d->dec_len);
   a.bf16 = d->dtype == PD_BF16;
   a.scale = scale_of(d);
   return hip_status(pd::launch_score_select(a, (hipStream_t)stream), "score/select kernels");
@@ -400,6 +399,7 @@ pd_status pd_sparse_decode_attn(const pd_dims* d, int32_t top_k, int32_t tok_bud
   a.Bt = tok_budget;
   a.n_static = n_static;
   a.S = S;
+  a.out_f32 = d->out_fp32;
   a.scale_log2 = scale_of(d) * 1.4426950408889634f;
   a.n_qt = decode_qtiles(d);
   a.total = decode_units(d) * S;
@@ -411,7 +411,8 @@ pd_status pd_sparse_decode_attn(const pd_dims* d, int32_t top_k, int32_t tok_bud
   hipError_t err = bf16 ? pd::launch_decode_bf16(a, d->head_dim, s) : pd::launch_decode_f32(a, d->head_dim, s);
   if (err != hipSuccess) return hip_status(err, "decode kernel");
   if (S > 1) {
-    err = pd::launch_merge(a.o_part, a.lse_part, o_dec, lse_dec, S, a.B, a.Hq, a.Ld, d->head_dim, bf16, s);
+    err = pd::launch_merge(a.o_part, a.lse_part, o_dec, lse_dec, S, a.B, a.Hq, a.Ld, d->head_dim,
+                           bf16 && !d->out_fp32, s);
     if (err != hipSuccess) return hip_status(err, "merge kernel");
   }
   return ok();

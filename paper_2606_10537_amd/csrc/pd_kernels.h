@@ -18,6 +18,7 @@ struct PrefillArgs {
   int B, N, C, Lq, Lm, Hq, Hkv, G, Sc;
   int n_qt, n_kvt, total;
   int qm_per_chunk;
+  int out_f32;       // o is fp32 instead of the input element type
   float scale_log2;  // softmax scale * log2(e)
 };
 
@@ -39,6 +40,7 @@ struct DecodeArgs {
   float* lse_part;   // [S][B][Hq][Ld] log2-domain shard LSE, S > 1
   int B, N, C, Hq, Hkv, G, Ld, Ls, K, Bt, n_static, S;
   int n_qt, total;
+  int out_f32;       // o_dec is fp32 instead of the input element type
   float scale_log2;
 };
 
@@ -62,14 +64,17 @@ hipError_t launch_merge(const float* o_part, const float* lse_part, void* o_dec,
 // Stage (b).
 struct SelectArgs {
   const void* q_dec;
-  const float *key_mean, *tok_score;
-  float* qbar;      // [B][Hq][D] workspace
-  float* scores;    // [B][N]
+  const float* key_mean;
+  const int32_t* tok_rank;
+  float* partial;   // [B][N][Hq*NS] workspace: per (head, row split) chunk-score terms
+  float* chunk_score;  // [B][N] or nullptr
   int32_t *chunk_idx, *tok_slot;
-  int B, N, C, Hq, Hkv, G, Ld, D, K, Bt;
+  int B, N, C, Hq, Hkv, G, Ld, D, K, Bt, NS;
   bool bf16;
   float scale;
 };
 hipError_t launch_score_select(const SelectArgs& a, hipStream_t s);
+hipError_t launch_token_rank(const float* tok_score, int32_t* tok_rank, int B, int N, int C, hipStream_t s);
+int select_row_splits(int Ld);
 
 }  // namespace pd

@@ -1,11 +1,18 @@
-// Stage (b): per-step chunk scores, top-K chunks and top-B_tok tokens per kept
-// chunk.  Three launches:
-//   1. qbar:   grid (b, h)  -- mean decode query of each head (fp32);
-//   2. scores: grid (b, n)  -- s[b][n] = scale * sum_h <qbar[b][h], key_mean[b][n][h/G]>;
-//   3. select: grid (b, k)  -- every workgroup ranks the N chunk scores (bitonic
-//      sort of (score desc, index asc) keys in LDS), takes the k-th kept chunk in
-//      ascending index order, ranks its C token scores the same way and writes
-//      the kept slots in ascending order (flags + block scan).
+// Stage (b): per-step chunk scores, top-K chunks and the kept tokens of each
+// kept chunk, plus the once-per-layer token ranking of stage (a).
+//
+//   token_rank: grid (b, n)     -- bitonic sort of the C Eq. 5 scores in LDS
+//                                  (score desc, index asc) -> rank of each token;
+//   qscore:     grid (b, h, sp) -- by linearity the chunk score splits into
+//                                  terms scale * <(1/L_d) sum_{r in sp} q_r, kbar_n>
+//                                  over heads and row splits: one workgroup sums
+//                                  its rows of one head, then dots with all N
+//                                  key means of that head's KV group;
+//   select:     grid (b, k)     -- sums the terms of every chunk in a fixed
+//                                  order, ranks the N scores (bitonic sort in
+//                                  LDS), takes the k-th kept chunk in ascending
+//                                  order and writes its tokens with rank < B_tok
+//                                  in ascending slot order (flags + block scan).
 // All reductions run in a fixed order, so results are bitwise reproducible.
 #include "pd_common.h"
 #include "pd_kernels.h"
@@ -61,39 +68,10 @@ __device__ void rows_mean(const void* src, size_t base_off, size_t row_stride, i
 }
 
 template <bool BF16>
-__global__ __launch_bounds__(256) void qbar_kernel(const void* q_dec, float* qbar, int Ld, int Hq, int D) {
-  __shared__ float red[2048];  // >= (256 / TPR) * D for d <= 128
-  const int b = blockIdx.x / Hq, h = blockIdx.x % Hq;
-  rows_mean<BF16>(q_dec, ((size_t)b * Ld * Hq + h) * D, (size_t)Hq * D, Ld, D, 1.0f / Ld,
-                  qbar + ((size_t)b * Hq + h) * D, red);
-}
-
-template <bool BF16>
 __global__ __launch_bounds__(256) void key_mean_kernel(const void* k_cache, float* key_mean, int C, int D) {
   __shared__ float red[2048];
   const size_t bng = blockIdx.x;  // ((b*N + n)*Hkv + g)
   rows_mean<BF16>(k_cache, (bng * (C + 1) + 1) * D, (size_t)D, C, D, 1.0f / C, key_mean + bng * D, red);
-}
-
-__global__ __launch_bounds__(256) void chunk_score_kernel(const float* qbar, const float* key_mean,
-                                                           float* scores, int N, int Hq, int Hkv,
-                                                           int G, int D, float scale) {
-  __shared__ float red[256];
-  const int b = blockIdx.x / N, n = blockIdx.x % N;
-  const float* qb = qbar + (size_t)b * Hq * D;
-  const float* kb = key_mean + ((size_t)b * N + n) * Hkv * D;
-  float acc = 0.f;
-  for (int i = threadIdx.x; i < Hq * D; i += 256) {
-    const int h = i / D, dd = i - h * D;
-    acc += qb[i] * kb[(h / G) * D + dd];
-  }
-  red[threadIdx.x] = acc;
-  __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
-    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) scores[(size_t)b * N + n] = red[0] * scale;
 }
 
 __device__ __forceinline__ uint64_t rank_key(float score, int idx) {
@@ -120,22 +98,86 @@ __device__ void bitonic_sort(uint64_t* keys, int P) {
   }
 }
 
-__global__ __launch_bounds__(256) void select_kernel(const float* scores, const float* tok_score,
-                                                      int32_t* chunk_idx, int32_t* tok_slot, int N,
-                                                      int C, int K, int Bt, int Npad, int Cpad) {
-  extern __shared__ __attribute__((aligned(16))) uint64_t sh[];
+static int next_pow2(int x) {
+  int p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+// Rank of every token of one chunk by its Eq. 5 score.
+__global__ __launch_bounds__(256) void token_rank_kernel(const float* tok_score, int32_t* tok_rank, int C,
+                                                          int Cpad) {
+  extern __shared__ __attribute__((aligned(16))) uint64_t keys[];
+  const size_t bn = blockIdx.x;
+  const float* e = tok_score + bn * C;
+  for (int j = threadIdx.x; j < Cpad; j += 256) keys[j] = j < C ? rank_key(e[j], j) : ~0ull;
+  __syncthreads();
+  bitonic_sort(keys, Cpad);
+  for (int i = threadIdx.x; i < C; i += 256) tok_rank[bn * C + (uint32_t)keys[i]] = i;
+}
+
+hipError_t launch_token_rank(const float* tok_score, int32_t* tok_rank, int B, int N, int C, hipStream_t s) {
+  const int Cpad = next_pow2(C);
+  hipLaunchKernelGGL(token_rank_kernel, dim3(B * N), dim3(256), (size_t)Cpad * 8, s, tok_score, tok_rank, C, Cpad);
+  return hipGetLastError();
+}
+
+// Decode rows per score workgroup.
+constexpr int kScoreRows = 128;
+int select_row_splits(int Ld) { return (Ld + kScoreRows - 1) / kScoreRows; }
+
+// Chunk-score terms of one (b, h, row split): scale * <(1/L_d) sum_r q_r, kbar[b][n][h/G]> for all n.
+template <bool BF16>
+__global__ __launch_bounds__(256) void qscore_kernel(const void* q_dec, const float* key_mean, float* partial,
+                                                      int N, int Hq, int Hkv, int G, int Ld, int D, int NS,
+                                                      float scale) {
+  __shared__ float red[2048];
+  __shared__ float qp[128];
+  const int sp = blockIdx.x % NS;
+  const int bh = blockIdx.x / NS;
+  const int h = bh % Hq, b = bh / Hq;
+  const int r0 = sp * kScoreRows, r1 = min(Ld, r0 + kScoreRows);
+  rows_mean<BF16>(q_dec, (((size_t)b * Ld + r0) * Hq + h) * D, (size_t)Hq * D, r1 - r0, D, 1.0f / Ld, qp, red);
+  __syncthreads();
+  const float* kb = key_mean + ((size_t)b * N * Hkv + h / G) * D;
+  for (int n = threadIdx.x; n < N; n += 256) {
+    const f32x4* kr = reinterpret_cast<const f32x4*>(kb + (size_t)n * Hkv * D);
+    float acc = 0.f;
+    for (int i = 0; i < D / 4; ++i) {
+      const f32x4 v = kr[i];
+      acc = fmaf(qp[4 * i], v[0], acc);
+      acc = fmaf(qp[4 * i + 1], v[1], acc);
+      acc = fmaf(qp[4 * i + 2], v[2], acc);
+      acc = fmaf(qp[4 * i + 3], v[3], acc);
+    }
+    partial[((size_t)b * N + n) * Hq * NS + (size_t)h * NS + sp] = acc * scale;
+  }
+}
+
+__global__ __launch_bounds__(256) void select_kernel(const float* partial, const int32_t* tok_rank,
+                                                      float* chunk_score, int32_t* chunk_idx, int32_t* tok_slot,
+                                                      int N, int C, int K, int Bt, int T, int Npad) {
+  extern __shared__ __attribute__((aligned(16))) uint64_t keys[];
   __shared__ int my_chunk;
   __shared__ int scan[2][256];
-  const int P = Npad > Cpad ? Npad : Cpad;
-  uint64_t* keys = sh;
-  int* flag = reinterpret_cast<int*>(sh + P);
   const int b = blockIdx.x / K, k = blockIdx.x % K;
   const int t = threadIdx.x;
 
-  // Top-K chunks.
-  for (int i = t; i < Npad; i += 256) keys[i] = i < N ? rank_key(scores[(size_t)b * N + i], i) : ~0ull;
+  // Chunk scores: the T = Hq*NS terms of each chunk summed in order.
+  for (int n = t; n < Npad; n += 256) {
+    if (n < N) {
+      const float* pr = partial + ((size_t)b * N + n) * T;
+      float s = 0.f;
+      for (int j = 0; j < T; ++j) s += pr[j];
+      keys[n] = rank_key(s, n);
+      if (k == 0 && chunk_score) chunk_score[(size_t)b * N + n] = s;
+    } else {
+      keys[n] = ~0ull;
+    }
+  }
   __syncthreads();
   bitonic_sort(keys, Npad);
+  // The K kept chunks (first K keys) in ascending index order.
   for (int i = t; i < K; i += 256) {
     const int x = (int)(uint32_t)keys[i];
     int pos = 0;
@@ -144,25 +186,14 @@ __global__ __launch_bounds__(256) void select_kernel(const float* scores, const 
     if (k == 0) chunk_idx[(size_t)b * K + pos] = x;
   }
   __syncthreads();
-  const int n = my_chunk;
-  __syncthreads();
+  const int32_t* rk = tok_rank + ((size_t)b * N + my_chunk) * C;
 
-  // Top-Bt tokens of chunk n.
-  const float* e = tok_score + ((size_t)b * N + n) * C;
-  for (int j = t; j < Cpad; j += 256) {
-    keys[j] = j < C ? rank_key(e[j], j) : ~0ull;
-    flag[j] = 0;
-  }
-  __syncthreads();
-  bitonic_sort(keys, Cpad);
-  for (int i = t; i < Bt; i += 256) flag[(uint32_t)keys[i]] = 1;
-  __syncthreads();
-
-  // Exclusive scan of the flags over contiguous segments of C.
+  // Kept tokens (rank < Bt) in ascending order: counts over contiguous segments,
+  // an exclusive block scan, then each segment writes its slots.
   const int seg = (C + 255) / 256;
   const int j0 = t * seg, j1 = min(C, j0 + seg);
   int cnt = 0;
-  for (int j = j0; j < j1; ++j) cnt += flag[j];
+  for (int j = j0; j < j1; ++j) cnt += rk[j] < Bt;
   scan[0][t] = cnt;
   __syncthreads();
   int cur = 0;
@@ -175,31 +206,22 @@ __global__ __launch_bounds__(256) void select_kernel(const float* scores, const 
   int pos = scan[cur][t] - cnt;
   int32_t* out = tok_slot + ((size_t)b * K + k) * Bt;
   for (int j = j0; j < j1; ++j)
-    if (flag[j]) out[pos++] = j + 1;
-}
-
-static int next_pow2(int x) {
-  int p = 1;
-  while (p < x) p <<= 1;
-  return p;
+    if (rk[j] < Bt) out[pos++] = j + 1;
 }
 
 hipError_t launch_score_select(const SelectArgs& a, hipStream_t s) {
+  const dim3 g1(a.B * a.Hq * a.NS);
   if (a.bf16)
-    hipLaunchKernelGGL(qbar_kernel<true>, dim3(a.B * a.Hq), dim3(256), 0, s, a.q_dec, a.qbar, a.Ld, a.Hq, a.D);
+    hipLaunchKernelGGL(qscore_kernel<true>, g1, dim3(256), 0, s, a.q_dec, a.key_mean, a.partial, a.N, a.Hq, a.Hkv,
+                       a.G, a.Ld, a.D, a.NS, a.scale);
   else
-    hipLaunchKernelGGL(qbar_kernel<false>, dim3(a.B * a.Hq), dim3(256), 0, s, a.q_dec, a.qbar, a.Ld, a.Hq, a.D);
+    hipLaunchKernelGGL(qscore_kernel<false>, g1, dim3(256), 0, s, a.q_dec, a.key_mean, a.partial, a.N, a.Hq, a.Hkv,
+                       a.G, a.Ld, a.D, a.NS, a.scale);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(chunk_score_kernel, dim3(a.B * a.N), dim3(256), 0, s, a.qbar, a.key_mean, a.scores,
-                     a.N, a.Hq, a.Hkv, a.G, a.D, a.scale);
-  err = hipGetLastError();
-  if (err != hipSuccess) return err;
-  const int Npad = next_pow2(a.N), Cpad = next_pow2(a.C);
-  const int P = Npad > Cpad ? Npad : Cpad;
-  const size_t lds = (size_t)P * 8 + (size_t)P * 4;
-  hipLaunchKernelGGL(select_kernel, dim3(a.B * a.K), dim3(256), lds, s, a.scores, a.tok_score, a.chunk_idx,
-                     a.tok_slot, a.N, a.C, a.K, a.Bt, Npad, Cpad);
+  const int Npad = next_pow2(a.N);
+  hipLaunchKernelGGL(select_kernel, dim3(a.B * a.K), dim3(256), (size_t)Npad * 8, s, a.partial, a.tok_rank,
+                     a.chunk_score, a.chunk_idx, a.tok_slot, a.N, a.C, a.K, a.Bt, a.Hq * a.NS, Npad);
   return hipGetLastError();
 }
 

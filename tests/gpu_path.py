@@ -27,34 +27,38 @@ def workspace(nbytes, device="cuda"):
 def run_prefill(d: Dims, x, stream=None):
     dev, dt = x["q_pre"].device, x["q_pre"].dtype
     B, N, C, Hq, Hkv, D = d.batch, d.n_chunks, d.chunk_len, d.n_heads_q, d.n_heads_kv, d.head_dim
+    odt = torch.float32 if d.out_fp32 else dt
     out = {
-        "o": torch.full((B, N, d.seq_len, Hq, D), float("nan"), dtype=dt, device=dev),
+        "o": torch.full((B, N, d.seq_len, Hq, D), float("nan"), dtype=odt, device=dev),
         "k_cache": torch.full((B, N, Hkv, C + 1, D), float("nan"), dtype=dt, device=dev),
         "v_cache": torch.full((B, N, Hkv, C + 1, D), float("nan"), dtype=dt, device=dev),
         "tok_score": torch.full((B, N, C), float("nan"), dtype=torch.float32, device=dev),
+        "tok_rank": torch.full((B, N, C), -1, dtype=torch.int32, device=dev),
         "key_mean": torch.full((B, N, Hkv, D), float("nan"), dtype=torch.float32, device=dev),
     }
     ws = workspace(_lib.pd_workspace_bytes(d, which=0), dev)
     _lib.pd_prefill_chunks(d, x["q_pre"], x["k_pre"], x["v_pre"], x["q_qm"], x["k_qm"], x["v_qm"],
-                           out["o"], out["k_cache"], out["v_cache"], out["tok_score"], out["key_mean"], ws,
+                           out["o"], out["k_cache"], out["v_cache"], out["tok_score"], out["tok_rank"],
+                           out["key_mean"], ws,
                            stream)
     return out
 
 
-def run_select(d: Dims, top_k, tok_budget, q_dec, key_mean, tok_score, stream=None):
+def run_select(d: Dims, top_k, tok_budget, q_dec, key_mean, tok_rank, stream=None):
     dev = q_dec.device
     ci = torch.full((d.batch, top_k), -1, dtype=torch.int32, device=dev)
     ts = torch.full((d.batch, top_k, tok_budget), -1, dtype=torch.int32, device=dev)
     cs = torch.full((d.batch, d.n_chunks), float("nan"), dtype=torch.float32, device=dev)
     ws = workspace(_lib.pd_workspace_bytes(d, top_k, tok_budget, 0, 1), dev)
-    _lib.pd_score_select(d, top_k, tok_budget, q_dec, key_mean, tok_score, ci, ts, cs, ws, stream)
+    _lib.pd_score_select(d, top_k, tok_budget, q_dec, key_mean, tok_rank, ci, ts, cs, ws, stream)
     return ci, ts, cs
 
 
 def run_decode(d: Dims, top_k, tok_budget, dec, cache, ci, ts, k_static, v_static, n_static, num_splits=0,
                with_lse=True, stream=None):
     dev = dec["q_dec"].device
-    o = torch.full(dec["q_dec"].shape, float("nan"), dtype=dec["q_dec"].dtype, device=dev)
+    odt = torch.float32 if d.out_fp32 else dec["q_dec"].dtype
+    o = torch.full(dec["q_dec"].shape, float("nan"), dtype=odt, device=dev)
     lse = (torch.full((d.batch, d.n_heads_q, d.dec_len), float("nan"), dtype=torch.float32, device=dev)
            if with_lse else None)
     ws = workspace(_lib.pd_workspace_bytes(d, top_k, tok_budget, num_splits, 2), dev)
@@ -116,3 +120,15 @@ def check_topk_rule_a(x, got, k, band=1e-3):
     extra = [i for i in np.nonzero(pin_out)[0] if i in gs]
     assert not missing and not extra, f"rule A violated: missing {missing} extra {extra}"
     return int(n - pin_in.sum() - pin_out.sum())
+
+
+def check_rank_consistent(e_ref, rank, band=1e-3):
+    """GPU token ranks of one chunk: a permutation of 0..C-1 that orders every pair
+    whose oracle scores differ by more than `band` the same way as the oracle."""
+    e_ref = np.asarray(e_ref, dtype=np.float64)
+    rank = np.asarray(rank)
+    C = e_ref.shape[0]
+    assert np.array_equal(np.sort(rank), np.arange(C)), "ranks are not a permutation"
+    before = rank[:, None] < rank[None, :]            # i ranked before j
+    bad = before & (e_ref[None, :] - e_ref[:, None] > band)
+    assert not bad.any(), f"{int(bad.sum())} pairs ranked against the oracle's order"

@@ -203,10 +203,13 @@ def check_select_golden():
     ts = np.array(g["tok_score"], float)
     s = OS.chunk_scores_ref(q, km, g["dims"]["scale"])
     np.testing.assert_allclose(s[0], g["expect_scores"], atol=1e-12)
+    rank = OS.token_rank_ref(ts)
+    assert rank.tolist() == g["expect_tok_rank"]
     for case in g["cases"]:
         ci, tsl, _ = OS.score_select_ref(q, km, ts, case["top_k"], case["tok_budget"], g["dims"]["scale"])
         assert ci[0].tolist() == case["chunk_idx"], case
         assert tsl[0].tolist() == case["tok_slot"], case
+        assert OS.tokens_by_rank_ref(rank, ci, case["tok_budget"])[0].tolist() == case["tok_slot"], case
 
 
 def check_chunk_score_zero_query(seed):
@@ -263,6 +266,27 @@ def check_topk_bruteforce(seed):
             assert list(got) == sorted(got)
             stable = np.sort(np.argsort(-x, kind="stable")[:k])
             assert np.array_equal(got, stable)
+
+
+def check_token_rank(seed):
+    """Ranks against a library routine (numpy stable argsort of -e) and, on small
+    integer scores with many ties, against counting: rank_j = #{i: e_i > e_j or
+    (e_i = e_j and i < j)}; selecting ranks below B reproduces the top-B slots."""
+    rng = np.random.default_rng(seed)
+    e = rng.integers(0, 4, size=(2, 3, 9)).astype(np.float64)
+    r = OS.token_rank_ref(e)
+    for b in range(2):
+        for n in range(3):
+            cnt = [sum(1 for i in range(9) if e[b, n, i] > e[b, n, j] or (e[b, n, i] == e[b, n, j] and i < j))
+                   for j in range(9)]
+            assert r[b, n].tolist() == cnt
+            inv = np.empty(9, dtype=np.int64)
+            inv[np.argsort(-e[b, n], kind="stable")] = np.arange(9)
+            assert np.array_equal(r[b, n], inv)
+    ci = np.array([[0, 2], [1, 2]])
+    for bt in (1, 4, 9):
+        want = np.stack([np.stack([1 + OS.topk_ref(e[b, n], bt) for n in ci[b]]) for b in range(2)])
+        assert np.array_equal(OS.tokens_by_rank_ref(r, ci, bt), want)
 
 
 # ----------------------------------------------------------------------------- stage (c)

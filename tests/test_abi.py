@@ -52,7 +52,8 @@ def dims(**kw):
 
 
 def prefill(d, ws=A, wsn=1 << 30, **ptrs):
-    names = ["q_pre", "k_pre", "v_pre", "q_qm", "k_qm", "v_qm", "o", "k_cache", "v_cache", "tok_score", "key_mean"]
+    names = ["q_pre", "k_pre", "v_pre", "q_qm", "k_qm", "v_qm", "o", "k_cache", "v_cache", "tok_score", "tok_rank",
+             "key_mean"]
     args = [ptrs.get(n, A) for n in names]
     lib = _lib.load()
     dd = d.c() if d is not None else None
@@ -74,6 +75,7 @@ def test_prefill_validation(lib):
     assert prefill(dims(), q_pre=None) == 1
     assert b"q_pre" in lib.pd_last_error_message()
     assert prefill(dims(), key_mean=None) == 1
+    assert prefill(dims(), tok_rank=None) == 1
     assert prefill(dims(), o=MIS) == 4
     assert prefill(dims(), ws=None) == 5
     assert prefill(dims(), wsn=16) == 5

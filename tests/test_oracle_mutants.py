@@ -78,6 +78,16 @@ def _scores_wrong_group(q_dec, key_mean, scale=None):
     return s
 
 
+def _rank_high_first_tie(tok_score):
+    e = np.asarray(tok_score, np.float64)
+    rank = np.zeros(e.shape, np.int32)
+    for b in range(e.shape[0]):
+        for n in range(e.shape[1]):
+            order = np.lexsort((-np.arange(e.shape[2]), -e[b, n]))
+            rank[b, n, order] = np.arange(e.shape[2])
+    return rank
+
+
 _orig_rows = OD.decode_kv_rows
 
 
@@ -112,6 +122,8 @@ MUTANTS = [
      [C.check_prefill_golden, lambda: C.check_key_mean_const(9)]),
     ("ties to the higher index", OS, "topk_ref", _topk_high_index,
      [C.check_select_golden, lambda: C.check_topk_bruteforce(13)]),
+    ("token ranks break ties to the higher index", OS, "token_rank_ref", _rank_high_first_tie,
+     [C.check_select_golden, lambda: C.check_token_rank(16)]),
     ("query head mapped to the wrong KV head", OS, "chunk_scores_ref", _scores_wrong_group,
      [lambda: C.check_chunk_score_gqa_groups(12)]),
     ("decode drops the chunk BOS rows", OD, "decode_kv_rows", _rows_no_bos,

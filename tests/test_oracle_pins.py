@@ -60,6 +60,10 @@ def test_topk_bruteforce():
     C.check_topk_bruteforce(13)
 
 
+def test_token_rank():
+    C.check_token_rank(16)
+
+
 def test_decode_golden():
     C.check_decode_golden()
 
