@@ -76,6 +76,10 @@ def load(path: str = LIB_PATH):
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"HIP library not built: {path} (run __graft_entry__.build())")
+    # torch ships its own HIP runtime with the same soname; loading torch first
+    # makes libpd.so bind to that one copy, so streams and device pointers the
+    # caller gets from torch belong to the runtime that launches the kernels.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     vp, sz, i32, fp = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_void_p
     dp = ctypes.POINTER(PdDims)
