@@ -35,7 +35,37 @@ def parse():
     p.add_argument("--dec-pool", type=int, default=4, help="decode input slots per layer")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU time budget of the oracle sample")
+    p.add_argument("--calib-copy-mib", type=int, default=0,
+                   help="before timing, copy this many MiB once (a plain copy kernel of known size for "
+                        "calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     return p.parse_args()
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_traffic_32k_32layer_b8.md")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_10537_amd", "csrc", f)
+                  for f in ("attn_bf16.hip", "pd_common.h", "pd_kernels.h", "pd_api.hip")]
+
+
+def kernel_source_digest():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per decode launch from the committed rocprofv3 counter summary,
+    or None when the kernel source changed since the counters were taken."""
+    try:
+        text = open(TRAFFIC_FILE).read()
+    except OSError:
+        return None
+    vals = dict(l.split(":", 1) for l in text.splitlines()
+                if l.startswith(("kernel_source_sha256:", "traffic_bytes_per_launch:")))
+    if vals.get("kernel_source_sha256", "").strip() != kernel_source_digest():
+        return None
+    return int(float(vals["traffic_bytes_per_launch"]))
 
 
 def algorithmic(w, layers):
@@ -177,6 +207,12 @@ def main():
                     ev_dec[i][1].record(stream)
                 i += 1
 
+    if args.calib_copy_mib:
+        src = torch.empty(args.calib_copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for _ in range(args.warmup):
         one_step(False)
     torch.cuda.synchronize()
@@ -215,7 +251,8 @@ def main():
         roof = {"bound": "hbm", "achieved": round(dec_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                 "frac": round(dec_gbps / PEAK_HBM_GBPS, 4)}
     roof.update({"kernel": "decode_bf16_kernel<128> (pd_sparse_decode_attn, one launch per layer and step)",
-                 "traffic": None, "launch_ms": round(dec_kern_ms, 5), "flop_per_launch": dec_flop,
+                 "traffic": measured_traffic() if (args.workload == 5 and not args.layers) else None,
+                 "launch_ms": round(dec_kern_ms, 5), "flop_per_launch": dec_flop,
                  "bytes_per_launch": dec_bytes})
 
     res = {
