@@ -127,12 +127,14 @@ constexpr int kScoreRows = 128;
 int select_row_splits(int Ld) { return (Ld + kScoreRows - 1) / kScoreRows; }
 
 // Chunk-score terms of one (b, h, row split): scale * <(1/L_d) sum_r q_r, kbar[b][n][h/G]> for all n.
-template <bool BF16>
+// The dot products run 8 lanes per chunk (D/8 dimensions each, all loads in
+// flight at once), reduced by a fixed xor butterfly.
+template <bool BF16, int D>
 __global__ __launch_bounds__(256) void qscore_kernel(const void* q_dec, const float* key_mean, float* partial,
-                                                      int N, int Hq, int Hkv, int G, int Ld, int D, int NS,
-                                                      float scale) {
+                                                      int N, int Hq, int Hkv, int G, int Ld, int NS, float scale) {
+  constexpr int SL = D / 8;
   __shared__ float red[2048];
-  __shared__ float qp[128];
+  __shared__ float qp[D];
   const int sp = blockIdx.x % NS;
   const int bh = blockIdx.x / NS;
   const int h = bh % Hq, b = bh / Hq;
@@ -140,17 +142,27 @@ __global__ __launch_bounds__(256) void qscore_kernel(const void* q_dec, const fl
   rows_mean<BF16>(q_dec, (((size_t)b * Ld + r0) * Hq + h) * D, (size_t)Hq * D, r1 - r0, D, 1.0f / Ld, qp, red);
   __syncthreads();
   const float* kb = key_mean + ((size_t)b * N * Hkv + h / G) * D;
-  for (int n = threadIdx.x; n < N; n += 256) {
-    const f32x4* kr = reinterpret_cast<const f32x4*>(kb + (size_t)n * Hkv * D);
+  const int j = threadIdx.x & 7;
+  float q[SL];
+#pragma unroll
+  for (int i = 0; i < SL; ++i) q[i] = qp[j * SL + i];
+  for (int n0 = 0; n0 < N; n0 += 32) {
+    const int n = n0 + (threadIdx.x >> 3);
     float acc = 0.f;
-    for (int i = 0; i < D / 4; ++i) {
-      const f32x4 v = kr[i];
-      acc = fmaf(qp[4 * i], v[0], acc);
-      acc = fmaf(qp[4 * i + 1], v[1], acc);
-      acc = fmaf(qp[4 * i + 2], v[2], acc);
-      acc = fmaf(qp[4 * i + 3], v[3], acc);
+    if (n < N) {
+      const f32x4* kr = reinterpret_cast<const f32x4*>(kb + (size_t)n * Hkv * D + j * SL);
+      f32x4 v[SL / 4];
+#pragma unroll
+      for (int i = 0; i < SL / 4; ++i) v[i] = kr[i];
+#pragma unroll
+      for (int i = 0; i < SL / 4; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc = fmaf(q[4 * i + e], v[i][e], acc);
     }
-    partial[((size_t)b * N + n) * Hq * NS + (size_t)h * NS + sp] = acc * scale;
+    acc += __shfl_xor(acc, 1);
+    acc += __shfl_xor(acc, 2);
+    acc += __shfl_xor(acc, 4);
+    if (j == 0 && n < N) partial[((size_t)b * N + n) * Hq * NS + (size_t)h * NS + sp] = acc * scale;
   }
 }
 
@@ -163,16 +175,27 @@ __global__ __launch_bounds__(256) void select_kernel(const float* partial, const
   const int b = blockIdx.x / K, k = blockIdx.x % K;
   const int t = threadIdx.x;
 
-  // Chunk scores: the T = Hq*NS terms of each chunk summed in order.
-  for (int n = t; n < Npad; n += 256) {
-    if (n < N) {
-      const float* pr = partial + ((size_t)b * N + n) * T;
+  // Chunk scores: the T = Hq*NS terms of each chunk, 8 lanes per chunk (lane j
+  // sums terms j, j+8, ...), then a fixed xor butterfly over the 8 lanes.
+  for (int n = t; n < Npad; n += 256) keys[n] = ~0ull;
+  __syncthreads();
+  {
+    const int j = t & 7;
+    for (int n0 = 0; n0 < N; n0 += 32) {
+      const int n = n0 + (t >> 3);
       float s = 0.f;
-      for (int j = 0; j < T; ++j) s += pr[j];
-      keys[n] = rank_key(s, n);
-      if (k == 0 && chunk_score) chunk_score[(size_t)b * N + n] = s;
-    } else {
-      keys[n] = ~0ull;
+      if (n < N) {
+        const float* pr = partial + ((size_t)b * N + n) * T;
+#pragma unroll 8
+        for (int i = j; i < T; i += 8) s += pr[i];
+      }
+      s += __shfl_xor(s, 1);
+      s += __shfl_xor(s, 2);
+      s += __shfl_xor(s, 4);
+      if (j == 0 && n < N) {
+        keys[n] = rank_key(s, n);
+        if (k == 0 && chunk_score) chunk_score[(size_t)b * N + n] = s;
+      }
     }
   }
   __syncthreads();
@@ -211,12 +234,15 @@ __global__ __launch_bounds__(256) void select_kernel(const float* partial, const
 
 hipError_t launch_score_select(const SelectArgs& a, hipStream_t s) {
   const dim3 g1(a.B * a.Hq * a.NS);
-  if (a.bf16)
-    hipLaunchKernelGGL(qscore_kernel<true>, g1, dim3(256), 0, s, a.q_dec, a.key_mean, a.partial, a.N, a.Hq, a.Hkv,
-                       a.G, a.Ld, a.D, a.NS, a.scale);
-  else
-    hipLaunchKernelGGL(qscore_kernel<false>, g1, dim3(256), 0, s, a.q_dec, a.key_mean, a.partial, a.N, a.Hq, a.Hkv,
-                       a.G, a.Ld, a.D, a.NS, a.scale);
+#define PD_QSCORE(BF, DD)                                                                                      \
+  hipLaunchKernelGGL((qscore_kernel<BF, DD>), g1, dim3(256), 0, s, a.q_dec, a.key_mean, a.partial, a.N, a.Hq, \
+                     a.Hkv, a.G, a.Ld, a.NS, a.scale)
+  if (a.D == 128) {
+    if (a.bf16) PD_QSCORE(true, 128); else PD_QSCORE(false, 128);
+  } else {
+    if (a.bf16) PD_QSCORE(true, 64); else PD_QSCORE(false, 64);
+  }
+#undef PD_QSCORE
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const int Npad = next_pow2(a.N);
