@@ -1,44 +1,68 @@
 // bf16 attention kernels for gfx950: chunk prefill (stage a) and sparse decode
 // attention (stage c).  Both run one tile engine:
 //
-//   * a workgroup = 4 waves = 128 query rows (32 per wave), d = 64 or 128;
-//   * K/V tiles of 64 rows are staged through LDS (K row-major, V transposed);
+//   * a workgroup = kBf16Waves waves (32 query rows each), d = 64 or 128;
+//   * K/V tiles of 64 rows go from HBM straight into LDS with
+//     global_load_lds_dwordx4 (no register staging), kBf16Stages tiles
+//     resident: the next ones stream in while the oldest is multiplied;
+//   * both tiles are stored row-major with an XOR swizzle of their 16-byte
+//     chunks, so that the K fragment reads (ds_read_b128) and the transposing
+//     V reads (ds_read_b64_tr_b16) are free of bank conflicts;
 //   * S^T = K Q^T and O^T += V^T P^T run on v_mfma_f32_32x32x16_bf16 with
 //     fp32 accumulation; Q stays in registers for the whole sweep;
 //   * online softmax in the log2 domain, lazy rescaling of the running output
 //     (only when a row maximum grows by more than 2^8), P rounded to bf16.
 //
 // Computing S transposed makes the MFMA output layout (each lane: one query,
-// 16 keys) directly usable as the B operand of the P*V product: the keys a
-// lane holds become its contraction slice, and the V^T operand is read in the
-// same key order by storing V^T in LDS with key bits 2 and 3 swapped.
+// 16 keys) directly usable as the B operand of the P*V product.  The matching
+// V^T operand (each lane: one d column, 8 keys) is produced from row-major V
+// by ds_read_b64_tr_b16: within a group of 16 lanes, lane j receives element
+// m of the 4 elements read by lane 4m + j/4, element j % 4.  If lane k of the
+// group points at V[key0 + k/4][d0 + 4(k%4)], lane j therefore receives
+// V[key0 + m][d0 + j], m = 0..3: four consecutive keys of one column.
 #include "pd_common.h"
 #include "pd_kernels.h"
 
 namespace pd {
 
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
+#define PD_LDS __attribute__((address_space(3)))
+
 template <int D>
 struct Tile {
-  static constexpr int BM = 128;             // query rows per workgroup
+  static constexpr int NW = kBf16Waves;      // waves per workgroup
+  static constexpr int BM = kBf16Rows;       // query rows per workgroup
   static constexpr int BN = 64;              // key rows per KV tile
-  static constexpr int NT = 256;             // threads per workgroup
+  static constexpr int NT = 64 * NW;         // threads per workgroup
+  static constexpr int S = kBf16Stages;      // resident K/V tiles
   static constexpr int CH = D / 8;           // 16-byte chunks per row
-  static constexpr int RPT = BN * CH / NT;   // rows each thread stages per tile
+  static constexpr int RPB = 64 / CH;        // rows per 1 KB DMA block (64 lanes x 16 B)
+  static constexpr int BPW = BN / RPB / NW;  // DMA blocks per wave and tile, for K and for V
   static constexpr int KS = D / 16;          // MFMA k-steps along d
   static constexpr int DB = D / 32;          // 32-row blocks of O^T
-  static constexpr int KPAD = D + 8;         // K row stride in LDS (elements)
-  static constexpr int VPAD = BN + 8;        // V^T row stride in LDS (elements)
-  static_assert(RPT == 2 || RPT == 4, "unsupported head dim");
+  static constexpr int TILE = BN * D;        // elements of one K or V tile
+  static_assert(BPW >= 1, "unsupported head dim");
 };
 
-// Column of key k (0..63) inside a V^T row: bits 2 and 3 swapped, so that the
-// 8 keys one lane contracts over in a k-step are 16 contiguous bytes.
-__device__ __forceinline__ int vt_col(int k) {
-  return (k & ~12) | ((k & 4) << 1) | ((k & 8) >> 1);
-}
+// Physical chunk of logical 16-byte chunk c of tile row r.  K: 8 consecutive
+// rows read the same logical chunk in one ds_read_b128 phase, so the chunk is
+// XORed with r % 8.  V: a transposing read covers 4 consecutive rows x 4
+// chunks per half wave; XOR with 4*(r % 2) spreads them over all banks.
+__device__ __forceinline__ int k_swz(int r) { return r & 7; }
+__device__ __forceinline__ int v_swz(int r) { return (r & 1) << 2; }
 
 __device__ __forceinline__ u32x4 ld16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ void st16(uint16_t* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+
+__device__ __forceinline__ i16x4 ld_tr16(const uint16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((PD_LDS i16x4*)(p));
+}
+
+// 16 bytes from global memory into LDS slot `lane` of the 1 KB block at lds.
+__device__ __forceinline__ void dma16(const uint16_t* g, uint16_t* lds) {
+  __builtin_amdgcn_global_load_lds(g, (PD_LDS void*)(lds), 16, 0, 0);
+}
 
 // Engine state of one wave: 32 query rows.
 template <int D>
@@ -51,50 +75,29 @@ struct WaveState {
   float qmass;  // this lane's partial mass on the query columns (prefill only)
 };
 
-// Thread -> (row group, 16-byte chunk) mappings used to stage a 64-row tile.
-// K: thread t takes chunk t % CH of rows RPT*(t / CH) .. +RPT-1 (row-major
-// stores, every bank hit equally often).  V: each wave takes all row groups
-// and CH/4 chunks, so that the 8 transposed stores of a thread (V^T rows 8c+e)
-// from one wave land on V^T rows whose 36-dword-strided bases alternate bank
-// halves: every bank is hit exactly twice per store instruction.
+// Lane-constant parts of the LDS fragment addresses (elements).
 template <int D>
-struct StageMap {
-  int rgk, ck, rgv, cv;
-  __device__ StageMap(int tid) {
+struct FragAddr {
+  int k;        // K row l32, chunk (grp ^ (l32 & 7)) for k-steps with ks % 4 == 0 ...
+  int kx;       // l32 & 7, the K swizzle of this lane's rows
+  int v[2];     // V transposing read: even / odd d blocks
+  __device__ FragAddr(int lane) {
     using T = Tile<D>;
-    const int lane = tid & 63, wave = tid >> 6, cpw = T::CH / 4;
-    ck = tid % T::CH;
-    rgk = tid / T::CH;
-    rgv = lane / cpw;
-    cv = wave * cpw + lane % cpw;
+    const int l32 = lane & 31, grp = lane >> 5;
+    kx = l32 & 7;
+    k = l32 * D;
+    (void)grp;
+    // Transposing V read: group q = lane / 16 of 16 lanes, kq = lane % 16.
+    // Key (tile row) 4*grp + kq/4 (+ 16 kk + 8 r2), d = 32 db + 16 (q % 2) + 4 (kq % 4).
+    const int kq = lane & 15, dh = (lane >> 4) & 1;
+    const int row = 4 * grp + (kq >> 2);
+    const int s = v_swz(row) >> 2;   // 1 when the row is odd
+    const int clo = 2 * dh + ((kq & 3) >> 1);
+#pragma unroll
+    for (int par = 0; par < 2; ++par)
+      v[par] = row * D + 8 * (4 * (par ^ s) + clo) + 4 * (kq & 1) - 32 * par;
   }
 };
-
-// Stage one K/V tile held in registers into LDS.
-template <int D>
-__device__ __forceinline__ void stage_tile(uint16_t* Ks, uint16_t* Vt, const StageMap<D>& mp,
-                                           const u32x4 (&kr)[Tile<D>::RPT],
-                                           const u32x4 (&vr)[Tile<D>::RPT]) {
-  using T = Tile<D>;
-#pragma unroll
-  for (int i = 0; i < T::RPT; ++i) st16(Ks + (mp.rgk * T::RPT + i) * T::KPAD + 8 * mp.ck, kr[i]);
-  const int col = vt_col(mp.rgv * T::RPT);
-  // Element e of each of the RPT rows, packed two halves per v_perm_b32:
-  // selector 0x05040100 takes the low halves of (lo, hi), 0x07060302 the high.
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int w = e >> 1;
-    const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
-    uint16_t* dst = Vt + (8 * mp.cv + e) * T::VPAD + col;
-    const uint32_t a = __builtin_amdgcn_perm(vr[1][w], vr[0][w], sel);
-    if constexpr (T::RPT == 4) {
-      const uint32_t b = __builtin_amdgcn_perm(vr[3][w], vr[2][w], sel);
-      *reinterpret_cast<u32x2*>(dst) = u32x2{a, b};
-    } else {
-      *reinterpret_cast<uint32_t*>(dst) = a;
-    }
-  }
-}
 
 // One KV tile for one wave: S^T = K Q^T, online softmax, O^T += V^T P^T.
 // kv_valid: number of valid keys in this tile (64 except in a ragged last tile).
@@ -103,8 +106,8 @@ __device__ __forceinline__ void stage_tile(uint16_t* Ks, uint16_t* Vt, const Sta
 // O is normalised by the sum of the same bf16-rounded weights that multiply V,
 // so rounding P perturbs a convex combination instead of scaling O.
 template <int D, bool EXACT>
-__device__ __forceinline__ void tile_step(WaveState<D>& st, const uint16_t* Ks, const uint16_t* Vt,
-                                          int l32, int grp, float scale_log2, int kv_valid,
+__device__ __forceinline__ void tile_step(WaveState<D>& st, const uint16_t* Ks, const uint16_t* Vs,
+                                          const FragAddr<D>& fa, int grp, float scale_log2, int kv_valid,
                                           int qlo, int qhi) {
   using T = Tile<D>;
   f32x16 s[2];
@@ -112,9 +115,10 @@ __device__ __forceinline__ void tile_step(WaveState<D>& st, const uint16_t* Ks, 
   for (int kb = 0; kb < 2; ++kb) s[kb] = f32x16{0};
 #pragma unroll
   for (int ks = 0; ks < T::KS; ++ks) {
+    const int c = (2 * ks + grp) ^ fa.kx;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-      bf16x8 a = __builtin_bit_cast(bf16x8, ld16(Ks + (32 * kb + l32) * T::KPAD + 16 * ks + 8 * grp));
+      bf16x8 a = __builtin_bit_cast(bf16x8, ld16(Ks + 32 * kb * D + fa.k + 8 * c));
       s[kb] = mfma32x32x16(a, st.qf[ks], s[kb]);
     }
   }
@@ -130,11 +134,13 @@ __device__ __forceinline__ void tile_step(WaveState<D>& st, const uint16_t* Ks, 
         s[kb][r] = key < kv_valid ? s[kb][r] : -INFINITY;
       }
   }
+  // One v_max3_f32 per pair (the file is built without NaN semantics, so no
+  // canonicalising v_max precedes each score).
   float mx = -INFINITY;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-    for (int r = 0; r < 16; r += 2) mx = fmaxf(mx, fmaxf(s[kb][r], s[kb][r + 1]));
+    for (int r = 0; r < 16; r += 2) mx = fmaxf(fmaxf(mx, s[kb][r]), s[kb][r + 1]);
   mx = fmaxf(mx, __shfl_xor(mx, 32)) * scale_log2;
   const bool upd = mx > st.m + 8.0f;
   if (__ballot(upd)) {
@@ -172,10 +178,6 @@ __device__ __forceinline__ void tile_step(WaveState<D>& st, const uint16_t* Ks, 
 #pragma unroll
   for (int i = 0; i < 16; ++i) lr = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[i]), ones, lr, false);
   st.l = lr;
-  bf16x8 pf[4];
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk)
-    pf[kk] = __builtin_bit_cast(bf16x8, u32x4{pk[4 * kk], pk[4 * kk + 1], pk[4 * kk + 2], pk[4 * kk + 3]});
   if (EXACT && qlo < qhi) {
     float qs = 0.f;
 #pragma unroll
@@ -187,12 +189,18 @@ __device__ __forceinline__ void tile_step(WaveState<D>& st, const uint16_t* Ks, 
       }
     st.qmass += qs;
   }
+  // P^T operand of k-step kk: keys 16kk + 4grp + {0..3} then 16kk + 8 + 4grp + {0..3}
+  // (pk[4kk .. 4kk+3]); the two transposing reads below deliver V^T in that order.
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk) {
+    const bf16x8 pf = __builtin_bit_cast(bf16x8, u32x4{pk[4 * kk], pk[4 * kk + 1], pk[4 * kk + 2], pk[4 * kk + 3]});
 #pragma unroll
     for (int db = 0; db < T::DB; ++db) {
-      bf16x8 a = __builtin_bit_cast(bf16x8, ld16(Vt + (32 * db + l32) * T::VPAD + 16 * kk + 8 * grp));
-      st.o[db] = mfma32x32x16(a, pf[kk], st.o[db]);
+      const uint16_t* vb = Vs + fa.v[db & 1] + 32 * db + 16 * kk * D;
+      const i16x4 lo = ld_tr16(vb);
+      const i16x4 hi = ld_tr16(vb + 8 * D);
+      const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      st.o[db] = mfma32x32x16(a, pf, st.o[db]);
     }
   }
 }
@@ -233,31 +241,78 @@ __device__ __forceinline__ void store_row_f32(float* dst, const WaveState<D>& st
     }
 }
 
-// Double-buffered sweep over KV tiles [t_begin, t_end): tile t is computed from
-// LDS buffer (t - t_begin) & 1 while tile t+1 is staged into the other buffer
-// and tile t+2 is already loading into registers; one barrier per tile.
-// load(t, kr, vr) fills the registers, hook(t, kr, vr) sees them before staging
-// (the prefill writes its cache share there), step(t, Ks, Vt) computes.
-template <int D, class Load, class Hook, class Step>
-__device__ __forceinline__ void kv_sweep(uint16_t* Ks0, uint16_t* Vt0, int t_begin, int t_end, const StageMap<D>& mp,
-                                         Load&& load, Hook&& hook, Step&& step) {
+// Global element pointers of one K row and one V row.
+struct RowPtr {
+  const uint16_t* k;
+  const uint16_t* v;
+};
+
+// Issue this wave's share of the DMA of one K/V tile: BPW blocks of RPB rows
+// each for K and for V.  row(r) returns the global K and V pointers of tile row
+// r (already clamped to a valid row); lane takes physical chunk lane % CH of
+// row r = block*RPB + lane / CH and loads the logical chunk that the swizzle
+// places there.  All row pointers are formed before the first DMA is issued:
+// an LDS read (a row table) after a DMA would make the compiler wait for it.
+template <int D, class Row>
+__device__ __forceinline__ void dma_tile(uint16_t* Kd, uint16_t* Vd, int wave, int lane, Row&& row) {
   using T = Tile<D>;
-  constexpr int KSZ = T::BN * T::KPAD, VSZ = D * T::VPAD;
-  u32x4 kr[T::RPT], vr[T::RPT];
-  load(t_begin, kr, vr);
-  hook(t_begin, kr, vr);
-  stage_tile<D>(Ks0, Vt0, mp, kr, vr);
-  if (t_begin + 1 < t_end) load(t_begin + 1, kr, vr);
-  __syncthreads();
-  for (int t = t_begin; t < t_end; ++t) {
-    const int cur = (t - t_begin) & 1;
-    step(t, Ks0 + cur * KSZ, Vt0 + cur * VSZ);
-    if (t + 1 < t_end) {
-      hook(t + 1, kr, vr);
-      stage_tile<D>(Ks0 + (cur ^ 1) * KSZ, Vt0 + (cur ^ 1) * VSZ, mp, kr, vr);
-      if (t + 2 < t_end) load(t + 2, kr, vr);
+  const int pc = lane % T::CH;
+  RowPtr rp[T::BPW];
+#pragma unroll
+  for (int j = 0; j < T::BPW; ++j) rp[j] = row((wave * T::BPW + j) * T::RPB + lane / T::CH);
+#pragma unroll
+  for (int j = 0; j < T::BPW; ++j) {
+    const int blk = wave * T::BPW + j;
+    const int r = blk * T::RPB + lane / T::CH;
+    dma16(rp[j].k + 8 * (pc ^ k_swz(r)), Kd + blk * 512);
+    dma16(rp[j].v + 8 * (pc ^ v_swz(r)), Vd + blk * 512);
+  }
+}
+
+// Wait until this wave has at most `newer` tiles of DMA in flight: tile DMAs
+// are loads and complete in issue order, so the tile issued before those has
+// landed (stores issued in between can only make the wait longer).
+template <int PER>
+__device__ __forceinline__ void wait_dma_keep(int newer) {
+  if (newer <= 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else if (newer == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(PER) : "memory");
+  else asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * PER) : "memory");
+}
+
+// Workgroup barrier without a memory fence.  __syncthreads() would also wait
+// for every LDS DMA still in flight (they count as outstanding LDS writes),
+// draining the pipeline; here the tile in use is covered by wait_dma_keep, and
+// every LDS read of older tiles has been consumed before a wave gets here.  The
+// memory clobber keeps the compiler from moving memory accesses across it.
+__device__ __forceinline__ void tile_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// Pipelined sweep over KV tiles [t_begin, t_end) with S resident tiles: tile t
+// lives in buffer (t - t_begin) % S; when it is computed, tiles t+1 .. t+S-2
+// are already in flight and t+S-1 is issued into the buffer of tile t-1.  One
+// barrier per tile: after it, tile t has landed for every wave and every wave
+// is done with tile t-1.  The buffers are distinct LDS objects and every
+// buffer index is a compile-time constant (the loop is unrolled by S), so the
+// compiler never mistakes a DMA into one buffer for a write to another.
+// dma(t, Kd, Vd) issues a tile, hook(t, Ks, Vs) sees a landed tile (the prefill
+// writes its cache share there), step(t, Ks, Vs) computes.
+template <int D, class Dma, class Hook, class Step>
+__device__ __forceinline__ void kv_sweep(uint16_t* const* Kb, uint16_t* const* Vb, int t_begin, int t_end, Dma&& dma, Hook&& hook, Step&& step) {
+  constexpr int S = Tile<D>::S, PER = 2 * Tile<D>::BPW;
+#pragma unroll
+  for (int i = 0; i < S - 1; ++i)
+    if (t_begin + i < t_end) dma(t_begin + i, Kb[i], Vb[i]);
+  for (int t = t_begin; t < t_end; t += S) {
+#pragma unroll
+    for (int i = 0; i < S; ++i) {
+      const int tt = t + i;
+      if (tt < t_end) {
+        wait_dma_keep<PER>(min(S - 2, t_end - 1 - tt));
+        tile_barrier();
+        if (tt + S - 1 < t_end) dma(tt + S - 1, Kb[(i + S - 1) % S], Vb[(i + S - 1) % S]);
+        hook(tt, Kb[i], Vb[i]);
+        step(tt, Kb[i], Vb[i]);
+      }
     }
-    __syncthreads();
   }
 }
 
@@ -267,12 +322,15 @@ __device__ __forceinline__ void kv_sweep(uint16_t* Ks0, uint16_t* Vt0, int t_beg
 // (b, n, kv-head) group), the per-head query-column mass of the content rows
 // and the log2-domain LSE of the query rows.
 template <int D>
-__global__ __launch_bounds__(256, 2) void prefill_bf16_kernel(PrefillArgs p) {
+__global__ __launch_bounds__(Tile<D>::NT, 8 / kBf16Waves) void prefill_bf16_kernel(PrefillArgs p) {
   using T = Tile<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2 * T::BN * T::KPAD];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[2 * D * T::VPAD];
+  __shared__ __attribute__((aligned(1024))) uint16_t K0[T::TILE], K1[T::TILE], K2[T::TILE], K3[T::TILE];
+  __shared__ __attribute__((aligned(1024))) uint16_t V0[T::TILE], V1[T::TILE], V2[T::TILE], V3[T::TILE];
+  uint16_t* const Kb[4] = {K0, K1, K2, K3};   // the first T::S are used
+  uint16_t* const Vb[4] = {V0, V1, V2, V3};
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, grp = lane >> 5;
   int lid = xcd_remap(blockIdx.x, p.total);
   const int qt = lid % p.n_qt;
@@ -299,8 +357,8 @@ __global__ __launch_bounds__(256, 2) void prefill_bf16_kernel(PrefillArgs p) {
       st.qf[ks] = src ? __builtin_bit_cast(bf16x8, ld16(src + 16 * ks + 8 * grp)) : bf16x8{0};
   }
   wave_init(st);
+  const FragAddr<D> fa(lane);
 
-  const StageMap<D> mp(tid);
   // Row r of the chunk sequence lives at base + r*HD (HD = H_kv*d elements), with
   // base the chunk's rows for r <= C and the shared query/pseudo-label rows after.
   // Rows past the end are clamped to the last row: their keys are masked out of
@@ -310,51 +368,41 @@ __global__ __launch_bounds__(256, 2) void prefill_bf16_kernel(PrefillArgs p) {
   const uint16_t* v_lo = p.v_pre + (chunk * C1 * p.Hkv + g) * D;
   const uint16_t* k_hi = p.k_qm + (qm_base * p.Hkv + g) * D - (size_t)C1 * HD;
   const uint16_t* v_hi = p.v_qm + (qm_base * p.Hkv + g) * D - (size_t)C1 * HD;
-  const int offk = mp.rgk * T::RPT * HD + 8 * mp.ck;   // this thread's first K row, within a tile
-  const int offv = mp.rgv * T::RPT * HD + 8 * mp.cv;
-  auto load = [&](int t, u32x4 (&kr)[T::RPT], u32x4 (&vr)[T::RPT]) {
+  auto dma = [&](int t, uint16_t* Kd, uint16_t* Vd) {
     const int r0 = t * T::BN;
-    if (r0 + T::BN <= C1 || (r0 >= C1 && r0 + T::BN <= p.Sc)) {
-      // Whole tile inside one source: rows r0.. at base + r0*HD, no per-row selects.
-      const uint16_t* kb = (r0 < C1 ? k_lo : k_hi) + (size_t)r0 * HD;
-      const uint16_t* vb = (r0 < C1 ? v_lo : v_hi) + (size_t)r0 * HD;
-#pragma unroll
-      for (int i = 0; i < T::RPT; ++i) {
-        kr[i] = ld16(kb + (unsigned)(offk + i * HD));
-        vr[i] = ld16(vb + (unsigned)(offv + i * HD));
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < T::RPT; ++i) {
-        const int rk = min(r0 + mp.rgk * T::RPT + i, p.Sc - 1);
-        const int rv = min(r0 + mp.rgv * T::RPT + i, p.Sc - 1);
-        kr[i] = ld16((rk < C1 ? k_lo : k_hi) + (unsigned)(rk * HD + 8 * mp.ck));
-        vr[i] = ld16((rv < C1 ? v_lo : v_hi) + (unsigned)(rv * HD + 8 * mp.cv));
-      }
-    }
+    dma_tile<D>(Kd, Vd, wave, lane, [=](int r) {
+      const int rr = min(r0 + r, p.Sc - 1);
+      const bool lo = rr < C1;
+      const unsigned off = (unsigned)rr * HD;
+      return RowPtr{(lo ? k_lo : k_hi) + off, (lo ? v_lo : v_hi) + off};
+    });
   };
   // Each KV tile of the (b, n, kv head) group is written to the cache by exactly
-  // one workgroup of that group: query tile t % n_qt of head g*G + (t / n_qt) % G.
-  auto cache_write = [&](int t, const u32x4 (&kr)[T::RPT], const u32x4 (&vr)[T::RPT]) {
+  // one workgroup of that group (query tile t % n_qt of head g*G + (t / n_qt) % G),
+  // from the landed LDS tile: thread tid copies logical chunks tid + NT i.
+  auto cache_write = [&](int t, const uint16_t* Ks, const uint16_t* Vs) {
     const bool writer = (t % p.n_qt == qt) && ((t / p.n_qt) % p.G == h % p.G);
     if (!writer) return;
     const size_t base = (chunk * p.Hkv + g) * C1;
 #pragma unroll
-    for (int i = 0; i < T::RPT; ++i) {
-      const int rk = t * T::BN + mp.rgk * T::RPT + i;
-      if (rk < C1) st16(p.k_cache + (base + rk) * D + 8 * mp.ck, kr[i]);
-      const int rv = t * T::BN + mp.rgv * T::RPT + i;
-      if (rv < C1) st16(p.v_cache + (base + rv) * D + 8 * mp.cv, vr[i]);
+    for (int i = 0; i < T::BN * T::CH / T::NT; ++i) {
+      const int u = tid + T::NT * i;
+      const int r = u / T::CH, c = u % T::CH;
+      const int row = t * T::BN + r;
+      if (row < C1) {
+        st16(p.k_cache + (base + row) * D + 8 * c, ld16(Ks + r * D + 8 * (c ^ k_swz(r))));
+        st16(p.v_cache + (base + row) * D + 8 * c, ld16(Vs + r * D + 8 * (c ^ v_swz(r))));
+      }
     }
   };
 
   const int qc_lo = C1, qc_hi = C1 + p.Lq;   // query columns counted by Eq. 5
-  kv_sweep<D>(Ks, Vt, 0, p.n_kvt, mp, load, cache_write, [&](int t, const uint16_t* ks, const uint16_t* vt) {
+  kv_sweep<D>(Kb, Vb, 0, p.n_kvt, dma, cache_write, [&](int t, const uint16_t* ks, const uint16_t* vs) {
     if (!wave_active) return;
     const int t0 = t * T::BN;
     const int kv_valid = min(T::BN, p.Sc - t0);
     const int lo = max(qc_lo - t0, 0), hi = min(qc_hi - t0, T::BN);
-    tile_step<D, true>(st, ks, vt, l32, grp, p.scale_log2, kv_valid, lo, hi);
+    tile_step<D, true>(st, ks, vs, fa, grp, p.scale_log2, kv_valid, lo, hi);
   });
   if (!wave_active) return;
 
@@ -380,13 +428,16 @@ __global__ __launch_bounds__(256, 2) void prefill_bf16_kernel(PrefillArgs p) {
 // is head g*G + rho / L_d, decode row rho % L_d.  KV row j of the shard walks:
 // [kept chunks: BOS + kept slots] ; [static rows] ; [own rows].
 template <int D>
-__global__ __launch_bounds__(256, 2) void decode_bf16_kernel(DecodeArgs p) {
+__global__ __launch_bounds__(Tile<D>::NT, 8 / kBf16Waves) void decode_bf16_kernel(DecodeArgs p) {
   using T = Tile<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2 * T::BN * T::KPAD];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[2 * D * T::VPAD];
+  __shared__ __attribute__((aligned(1024))) uint16_t K0[T::TILE], K1[T::TILE], K2[T::TILE], K3[T::TILE];
+  __shared__ __attribute__((aligned(1024))) uint16_t V0[T::TILE], V1[T::TILE], V2[T::TILE], V3[T::TILE];
+  uint16_t* const Kb[4] = {K0, K1, K2, K3};   // the first T::S are used
+  uint16_t* const Vb[4] = {V0, V1, V2, V3};
   __shared__ __attribute__((aligned(16))) int rowtab[kDecodeTableRows];   // cache row (n*Hkv*(C+1) + slot) of gathered rows
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, grp = lane >> 5;
   int lid = xcd_remap(blockIdx.x, p.total);
   const int sp = lid % p.S;
@@ -412,13 +463,13 @@ __global__ __launch_bounds__(256, 2) void decode_bf16_kernel(DecodeArgs p) {
       st.qf[ks] = src ? __builtin_bit_cast(bf16x8, ld16(src + 16 * ks + 8 * grp)) : bf16x8{0};
   }
   wave_init(st);
+  const FragAddr<D> fa(lane);
 
   // This shard's tiles.
   const int n_kvt = (L_kv + T::BN - 1) / T::BN;
   const int t_begin = (int)(((long long)n_kvt * sp) / p.S);
   const int t_end = (int)(((long long)n_kvt * (sp + 1)) / p.S);
 
-  const StageMap<D> mp(tid);
   const size_t cache_bg = ((size_t)b * p.N * p.Hkv + g) * C1;   // + n*Hkv*C1 + slot
   // Gathered rows of this shard: row codes into LDS once (the host keeps every
   // shard within kDecodeTableRows rows), so tile loads need no index fetch.
@@ -447,49 +498,37 @@ __global__ __launch_bounds__(256, 2) void decode_bf16_kernel(DecodeArgs p) {
   const uint16_t* kd_ = p.k_dec + db;
   const uint16_t* vd_ = p.v_dec + db;
   const int tab_hi = max(j_hi - j_lo - 1, 0);
-  auto row_ptr = [&](int j, const uint16_t* c_, const uint16_t* s_, const uint16_t* d_, int ch) {
-    j = min(j, L_kv - 1);
-    const unsigned tab = (unsigned)rowtab[min(max(j - j_lo, 0), tab_hi)] * D;
-    const uint16_t* base = j < n_sel ? c_ : (j < n_sel + p.n_static ? s_ : d_);
-    const unsigned off = j < n_sel ? tab : (unsigned)(j * HD);
-    return base + off + 8 * ch;
-  };
-  static_assert(T::RPT == 4 || T::RPT == 2, "");
-  auto load = [&](int t, u32x4 (&kr)[T::RPT], u32x4 (&vr)[T::RPT]) {
+  const int n_static = p.n_static;
+  int* const rowtab_p = rowtab;
+  auto dma = [=](int t, uint16_t* Kd, uint16_t* Vd) {
+    const int* rowtab = rowtab_p;
     const int r0 = t * T::BN;
     if (r0 + T::BN <= n_sel) {
-      // Whole tile gathered from the cache: the RPT row codes of a thread are
-      // consecutive table entries (one LDS read).
-      const int* tk = rowtab + (r0 - j_lo) + mp.rgk * T::RPT;
-      const int* tv = rowtab + (r0 - j_lo) + mp.rgv * T::RPT;
-      int ck[T::RPT], cv[T::RPT];
-      if constexpr (T::RPT == 4) {
-        const u32x4 a = *reinterpret_cast<const u32x4*>(tk), b = *reinterpret_cast<const u32x4*>(tv);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) { ck[i] = (int)a[i]; cv[i] = (int)b[i]; }
-      } else {
-        const u32x2 a = *reinterpret_cast<const u32x2*>(tk), b = *reinterpret_cast<const u32x2*>(tv);
-#pragma unroll
-        for (int i = 0; i < 2; ++i) { ck[i] = (int)a[i]; cv[i] = (int)b[i]; }
-      }
-#pragma unroll
-      for (int i = 0; i < T::RPT; ++i) {
-        kr[i] = ld16(kc + ((unsigned)ck[i] * D + 8 * mp.ck));
-        vr[i] = ld16(vc + ((unsigned)cv[i] * D + 8 * mp.cv));
-      }
+      // Whole tile gathered from the cache.
+      const int* tab = rowtab + (r0 - j_lo);
+      dma_tile<D>(Kd, Vd, wave, lane, [=](int r) {
+        const unsigned off = (unsigned)tab[r] * D;
+        return RowPtr{kc + off, vc + off};
+      });
     } else {
-#pragma unroll
-      for (int i = 0; i < T::RPT; ++i) {
-        kr[i] = ld16(row_ptr(r0 + mp.rgk * T::RPT + i, kc, ks_, kd_, mp.ck));
-        vr[i] = ld16(row_ptr(r0 + mp.rgv * T::RPT + i, vc, vs_, vd_, mp.cv));
-      }
+      dma_tile<D>(Kd, Vd, wave, lane, [=](int r) {
+        const int j = min(r0 + r, L_kv - 1);
+        const unsigned tab = (unsigned)rowtab[min(max(j - j_lo, 0), tab_hi)] * D;
+        const bool gath = j < n_sel, stat = j < n_sel + n_static;
+        const unsigned off = gath ? tab : (unsigned)(j * HD);
+        const uint16_t* kb = stat ? ks_ : kd_;
+        const uint16_t* vb = stat ? vs_ : vd_;
+        kb = gath ? kc : kb;
+        vb = gath ? vc : vb;
+        return RowPtr{kb + off, vb + off};
+      });
     }
   };
-  auto no_hook = [](int, const u32x4 (&)[T::RPT], const u32x4 (&)[T::RPT]) {};
-  kv_sweep<D>(Ks, Vt, t_begin, t_end, mp, load, no_hook, [&](int t, const uint16_t* ks, const uint16_t* vt) {
+  auto no_hook = [](int, const uint16_t*, const uint16_t*) {};
+  kv_sweep<D>(Kb, Vb, t_begin, t_end, dma, no_hook, [&](int t, const uint16_t* ks, const uint16_t* vs) {
     if (!wave_active) return;
     const int kv_valid = min(T::BN, L_kv - t * T::BN);
-    tile_step<D, false>(st, ks, vt, l32, grp, p.scale_log2, kv_valid, 0, 0);
+    tile_step<D, false>(st, ks, vs, fa, grp, p.scale_log2, kv_valid, 0, 0);
   });
   if (!wave_active || rho >= GL) return;
 
@@ -590,7 +629,7 @@ __global__ __launch_bounds__(256) void escore_bf16_kernel(EscoreArgs p) {
 // Host-side launchers.
 template <int D>
 static hipError_t launch_prefill_d(const PrefillArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(prefill_bf16_kernel<D>, dim3(a.total), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(prefill_bf16_kernel<D>, dim3(a.total), dim3(Tile<D>::NT), 0, s, a);
   return hipGetLastError();
 }
 hipError_t launch_prefill_bf16(const PrefillArgs& a, int head_dim, hipStream_t s) {
@@ -599,7 +638,7 @@ hipError_t launch_prefill_bf16(const PrefillArgs& a, int head_dim, hipStream_t s
 
 template <int D>
 static hipError_t launch_decode_d(const DecodeArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(decode_bf16_kernel<D>, dim3(a.total), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(decode_bf16_kernel<D>, dim3(a.total), dim3(Tile<D>::NT), 0, s, a);
   return hipGetLastError();
 }
 hipError_t launch_decode_bf16(const DecodeArgs& a, int head_dim, hipStream_t s) {

@@ -33,7 +33,7 @@ pd_status ok() {
 constexpr int kMaxChunks = 1024;
 constexpr int kMaxChunkLen = 4096;
 constexpr int kMaxSplits = 64;
-constexpr int kTargetWorkgroups = 512;  // two resident workgroups per CU on 256 CUs
+constexpr int kTargetWorkgroups = 256 * 8 / pd::kBf16Waves;  // two resident waves per SIMD on 256 CUs
 constexpr size_t kAlign = 256;
 
 size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -103,7 +103,7 @@ size_t select_ws(const pd_dims* d) {
 
 int decode_qtiles(const pd_dims* d) {
   const int G = d->n_heads_q / d->n_heads_kv;
-  return d->dtype == PD_BF16 ? cdiv((long long)G * d->dec_len, 128) : cdiv(d->dec_len, 64);
+  return d->dtype == PD_BF16 ? cdiv((long long)G * d->dec_len, pd::kBf16Rows) : cdiv(d->dec_len, 64);
 }
 int decode_units(const pd_dims* d) {
   return d->dtype == PD_BF16 ? d->batch * d->n_heads_kv * decode_qtiles(d)
@@ -259,7 +259,7 @@ pd_status pd_prefill_chunks(const pd_dims* d, const void* q_pre, const void* k_p
   a.qm_per_chunk = d->qm_per_chunk;
   a.out_f32 = d->out_fp32;
   a.scale_log2 = scale_of(d) * 1.4426950408889634f;
-  a.n_qt = cdiv(a.Sc, bf16 ? 128 : 64);
+  a.n_qt = cdiv(a.Sc, bf16 ? pd::kBf16Rows : 64);
   a.n_kvt = cdiv(a.Sc, 64);
   a.total = a.B * a.N * a.Hq * a.n_qt;
 
