@@ -45,12 +45,25 @@ struct Tile {
   static_assert(BPW >= 1, "unsupported head dim");
 };
 
-// Physical chunk of logical 16-byte chunk c of tile row r.  K: 8 consecutive
-// rows read the same logical chunk in one ds_read_b128 phase, so the chunk is
-// XORed with r % 8.  V: a transposing read covers 4 consecutive rows x 4
-// chunks per half wave; XOR with 4*(r % 2) spreads them over all banks.
-__device__ __forceinline__ int k_swz(int r) { return r & 7; }
-__device__ __forceinline__ int v_swz(int r) { return (r & 1) << 2; }
+// Physical chunk of logical 16-byte chunk c of tile row r.  LDS has 64 banks
+// (256 bytes per bank row); ds_read_b128 serves 16 lanes per pass and
+// ds_read_b64 32 lanes, and a pass is conflict-free when its lanes cover all
+// 256 bytes of a bank row.  K: the 16 lanes of a pass read one logical chunk
+// of 16 consecutive rows, so those rows must land on 16 distinct 16-byte bank
+// groups.  V: the 32 lanes of a transposing read cover 64 bytes (4 chunks) of
+// each of 4 consecutive rows, so those rows must land on 4 distinct 64-byte
+// bank groups.  With d = 128 a row is a whole bank row; with d = 64 two rows
+// share one, which the row bit 0 already separates.
+template <int D>
+__device__ __forceinline__ int k_swz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
+template <int D>
+__device__ __forceinline__ int v_swz(int r) { return D == 128 ? ((r & 3) << 2) : (((r >> 1) & 1) << 2); }
+
+// Wave group of a wave (0 or 1): one wave of each group per SIMD.
+#ifndef PD_GROUP_OF_WAVE
+#define PD_GROUP_OF_WAVE(w) ((w) >> 2)
+#endif
+__device__ __forceinline__ int wave_group(int wave) { return kBf16Waves == 8 ? PD_GROUP_OF_WAVE(wave) : 0; }
 
 __device__ __forceinline__ u32x4 ld16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ void st16(uint16_t* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
@@ -78,39 +91,36 @@ struct WaveState {
 // Lane-constant parts of the LDS fragment addresses (elements).
 template <int D>
 struct FragAddr {
-  int k;        // K row l32, chunk (grp ^ (l32 & 7)) for k-steps with ks % 4 == 0 ...
-  int kx;       // l32 & 7, the K swizzle of this lane's rows
-  int v[2];     // V transposing read: even / odd d blocks
+  int k;              // K: row l32 (+ 32 kb), logical chunk 2 ks + grp XOR kx
+  int kx;             // K swizzle of this lane's rows (rows 32 kb + l32 share it)
+  int v[D / 32];      // V transposing read of d block db: key row 4 grp + kq/4 (+ 16 kk + 8 r2)
   __device__ FragAddr(int lane) {
-    using T = Tile<D>;
     const int l32 = lane & 31, grp = lane >> 5;
-    kx = l32 & 7;
+    kx = k_swz<D>(l32);
     k = l32 * D;
-    (void)grp;
-    // Transposing V read: group q = lane / 16 of 16 lanes, kq = lane % 16.
-    // Key (tile row) 4*grp + kq/4 (+ 16 kk + 8 r2), d = 32 db + 16 (q % 2) + 4 (kq % 4).
+    // Group q = lane / 16 of 16 lanes, kq = lane % 16: this lane points at
+    // V[row][32 db + 16 (q % 2) + 4 (kq % 4)], 4 elements; the swizzle of row
+    // is the same for rows + 16 kk + 8 r2.
     const int kq = lane & 15, dh = (lane >> 4) & 1;
     const int row = 4 * grp + (kq >> 2);
-    const int s = v_swz(row) >> 2;   // 1 when the row is odd
     const int clo = 2 * dh + ((kq & 3) >> 1);
 #pragma unroll
-    for (int par = 0; par < 2; ++par)
-      v[par] = row * D + 8 * (4 * (par ^ s) + clo) + 4 * (kq & 1) - 32 * par;
+    for (int db = 0; db < D / 32; ++db) v[db] = row * D + 8 * ((4 * db + clo) ^ v_swz<D>(row)) + 4 * (kq & 1);
   }
 };
 
-// One KV tile for one wave: S^T = K Q^T, online softmax, O^T += V^T P^T.
-// kv_valid: number of valid keys in this tile (64 except in a ragged last tile).
-// qlo/qhi: key range (tile-relative) counted into qmass; empty when qlo >= qhi.
-// EXACT: also keep the unrounded row sum and the query-column mass (prefill).
-// O is normalised by the sum of the same bf16-rounded weights that multiply V,
-// so rounding P perturbs a convex combination instead of scaling O.
-template <int D, bool EXACT>
-__device__ __forceinline__ void tile_step(WaveState<D>& st, const uint16_t* Ks, const uint16_t* Vs,
-                                          const FragAddr<D>& fa, int grp, float scale_log2, int kv_valid,
-                                          int qlo, int qhi) {
+// One KV tile for one wave, in three phases: S^T = K Q^T (s_phase), online
+// softmax producing the bf16 weights P (softmax_phase), O^T += V^T P^T
+// (pv_phase).  kv_valid: number of valid keys in this tile (64 except in a
+// ragged last tile).  qlo/qhi: key range (tile-relative) counted into qmass;
+// empty when qlo >= qhi.  EXACT: also keep the unrounded row sum and the
+// query-column mass (prefill).  O is normalised by the sum of the same
+// bf16-rounded weights that multiply V, so rounding P perturbs a convex
+// combination instead of scaling O.
+template <int D>
+__device__ __forceinline__ void s_phase(f32x16 (&s)[2], const WaveState<D>& st, const uint16_t* Ks,
+                                        const FragAddr<D>& fa, int grp) {
   using T = Tile<D>;
-  f32x16 s[2];
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) s[kb] = f32x16{0};
 #pragma unroll
@@ -122,6 +132,12 @@ __device__ __forceinline__ void tile_step(WaveState<D>& st, const uint16_t* Ks, 
       s[kb] = mfma32x32x16(a, st.qf[ks], s[kb]);
     }
   }
+}
+
+template <int D, bool EXACT>
+__device__ __forceinline__ void softmax_phase(WaveState<D>& st, f32x16 (&s)[2], uint32_t (&pk)[16], int grp,
+                                              float scale_log2, int kv_valid, int qlo, int qhi) {
+  using T = Tile<D>;
   // Key of s[kb][r]: 32*kb + 8*(r/4) + 4*grp + r%4.  The max is taken on raw
   // scores (the scale is positive) and the scale is folded into one FMA:
   // p = exp2(s * scale_log2 - m).
@@ -158,7 +174,6 @@ __device__ __forceinline__ void tile_step(WaveState<D>& st, const uint16_t* Ks, 
       for (int r = 0; r < 16; ++r) st.o[db][r] *= alpha;
   }
   const float nm = -st.m;
-  uint32_t pk[16];
   float lsum = 0.f;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
@@ -189,20 +204,45 @@ __device__ __forceinline__ void tile_step(WaveState<D>& st, const uint16_t* Ks, 
       }
     st.qmass += qs;
   }
-  // P^T operand of k-step kk: keys 16kk + 4grp + {0..3} then 16kk + 8 + 4grp + {0..3}
-  // (pk[4kk .. 4kk+3]); the two transposing reads below deliver V^T in that order.
+}
+
+// P^T operand of k-step kk: keys 16kk + 4grp + {0..3} then 16kk + 8 + 4grp + {0..3}
+// (pk[4kk .. 4kk+3]); the two transposing reads deliver V^T in that order.
+template <int D>
+__device__ __forceinline__ void pv_phase(WaveState<D>& st, const uint32_t (&pk)[16], const uint16_t* Vs,
+                                         const FragAddr<D>& fa) {
+  using T = Tile<D>;
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk) {
     const bf16x8 pf = __builtin_bit_cast(bf16x8, u32x4{pk[4 * kk], pk[4 * kk + 1], pk[4 * kk + 2], pk[4 * kk + 3]});
 #pragma unroll
     for (int db = 0; db < T::DB; ++db) {
-      const uint16_t* vb = Vs + fa.v[db & 1] + 32 * db + 16 * kk * D;
+      const uint16_t* vb = Vs + fa.v[db] + 16 * kk * D;
       const i16x4 lo = ld_tr16(vb);
       const i16x4 hi = ld_tr16(vb + 8 * D);
       const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
       st.o[db] = mfma32x32x16(a, pf, st.o[db]);
     }
   }
+}
+
+// The tile step of one wave.  The two wave groups of a workgroup (one wave of
+// each per SIMD) run the phases in different orders so that one group's
+// softmax overlaps the other's MFMAs: group 0 does S, softmax, P*V of tile t;
+// group 1 first does the P*V of tile t-1 (its weights are still in pk), then
+// S and softmax of tile t, and the P*V of the last tile right after its
+// softmax.  The order of the online-softmax updates is the same in both
+// groups.  One code path with wave-uniform guards keeps a single pk array.
+template <int D, bool EXACT>
+__device__ __forceinline__ void wave_step(WaveState<D>& st, uint32_t (&pk)[16], bool deferred, bool first, bool last,
+                                          const uint16_t* Ks, const uint16_t* Vs, const uint16_t* Vs_prev,
+                                          const FragAddr<D>& fa, int grp, float scale_log2, int kv_valid, int qlo,
+                                          int qhi) {
+  f32x16 s[2];
+  if (deferred && !first) pv_phase<D>(st, pk, Vs_prev, fa);
+  s_phase<D>(s, st, Ks, fa, grp);
+  softmax_phase<D, EXACT>(st, s, pk, grp, scale_log2, kv_valid, qlo, qhi);
+  if (!deferred || last) pv_phase<D>(st, pk, Vs, fa);
 }
 
 template <int D>
@@ -264,8 +304,8 @@ __device__ __forceinline__ void dma_tile(uint16_t* Kd, uint16_t* Vd, int wave, i
   for (int j = 0; j < T::BPW; ++j) {
     const int blk = wave * T::BPW + j;
     const int r = blk * T::RPB + lane / T::CH;
-    dma16(rp[j].k + 8 * (pc ^ k_swz(r)), Kd + blk * 512);
-    dma16(rp[j].v + 8 * (pc ^ v_swz(r)), Vd + blk * 512);
+    dma16(rp[j].k + 8 * (pc ^ k_swz<D>(r)), Kd + blk * 512);
+    dma16(rp[j].v + 8 * (pc ^ v_swz<D>(r)), Vd + blk * 512);
   }
 }
 
@@ -287,30 +327,32 @@ __device__ __forceinline__ void wait_dma_keep(int newer) {
 __device__ __forceinline__ void tile_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
 // Pipelined sweep over KV tiles [t_begin, t_end) with S resident tiles: tile t
-// lives in buffer (t - t_begin) % S; when it is computed, tiles t+1 .. t+S-2
-// are already in flight and t+S-1 is issued into the buffer of tile t-1.  One
+// lives in buffer (t - t_begin) % S.  When tile t is computed, tile t-1 is still
+// resident (its V feeds the deferred P*V of wave group 1), t+1 .. t+PF-1 are in
+// flight and t+PF (PF = S-2) is issued into the buffer of tile t-2.  One
 // barrier per tile: after it, tile t has landed for every wave and every wave
-// is done with tile t-1.  The buffers are distinct LDS objects and every
+// is done with tile t-1's step.  The buffers are distinct LDS objects and every
 // buffer index is a compile-time constant (the loop is unrolled by S), so the
 // compiler never mistakes a DMA into one buffer for a write to another.
 // dma(t, Kd, Vd) issues a tile, hook(t, Ks, Vs) sees a landed tile (the prefill
-// writes its cache share there), step(t, Ks, Vs) computes.
+// writes its cache share there), step(t, Ks, Vs, Vs_prev, last) computes.
 template <int D, class Dma, class Hook, class Step>
-__device__ __forceinline__ void kv_sweep(uint16_t* const* Kb, uint16_t* const* Vb, int t_begin, int t_end, Dma&& dma, Hook&& hook, Step&& step) {
-  constexpr int S = Tile<D>::S, PER = 2 * Tile<D>::BPW;
+__device__ __forceinline__ void kv_sweep(uint16_t* const* Kb, uint16_t* const* Vb, int t_begin, int t_end,
+                                         Dma&& dma, Hook&& hook, Step&& step) {
+  constexpr int S = Tile<D>::S, PF = S - 2, PER = 2 * Tile<D>::BPW;
 #pragma unroll
-  for (int i = 0; i < S - 1; ++i)
+  for (int i = 0; i < PF; ++i)
     if (t_begin + i < t_end) dma(t_begin + i, Kb[i], Vb[i]);
   for (int t = t_begin; t < t_end; t += S) {
 #pragma unroll
     for (int i = 0; i < S; ++i) {
       const int tt = t + i;
       if (tt < t_end) {
-        wait_dma_keep<PER>(min(S - 2, t_end - 1 - tt));
+        wait_dma_keep<PER>(min(PF - 1, t_end - 1 - tt));
         tile_barrier();
-        if (tt + S - 1 < t_end) dma(tt + S - 1, Kb[(i + S - 1) % S], Vb[(i + S - 1) % S]);
+        if (tt + PF < t_end) dma(tt + PF, Kb[(i + PF) % S], Vb[(i + PF) % S]);
         hook(tt, Kb[i], Vb[i]);
-        step(tt, Kb[i], Vb[i]);
+        step(tt, Kb[i], Vb[i], Vb[(i + S - 1) % S], tt == t_end - 1);
       }
     }
   }
@@ -390,20 +432,24 @@ __global__ __launch_bounds__(Tile<D>::NT, 8 / kBf16Waves) void prefill_bf16_kern
       const int r = u / T::CH, c = u % T::CH;
       const int row = t * T::BN + r;
       if (row < C1) {
-        st16(p.k_cache + (base + row) * D + 8 * c, ld16(Ks + r * D + 8 * (c ^ k_swz(r))));
-        st16(p.v_cache + (base + row) * D + 8 * c, ld16(Vs + r * D + 8 * (c ^ v_swz(r))));
+        st16(p.k_cache + (base + row) * D + 8 * c, ld16(Ks + r * D + 8 * (c ^ k_swz<D>(r))));
+        st16(p.v_cache + (base + row) * D + 8 * c, ld16(Vs + r * D + 8 * (c ^ v_swz<D>(r))));
       }
     }
   };
 
   const int qc_lo = C1, qc_hi = C1 + p.Lq;   // query columns counted by Eq. 5
-  kv_sweep<D>(Kb, Vb, 0, p.n_kvt, dma, cache_write, [&](int t, const uint16_t* ks, const uint16_t* vs) {
-    if (!wave_active) return;
-    const int t0 = t * T::BN;
-    const int kv_valid = min(T::BN, p.Sc - t0);
-    const int lo = max(qc_lo - t0, 0), hi = min(qc_hi - t0, T::BN);
-    tile_step<D, true>(st, ks, vs, fa, grp, p.scale_log2, kv_valid, lo, hi);
-  });
+  uint32_t pk_prev[16];
+  const bool deferred = wave_group(wave) != 0;
+  kv_sweep<D>(Kb, Vb, 0, p.n_kvt, dma, cache_write,
+              [&](int t, const uint16_t* ks, const uint16_t* vs, const uint16_t* vs_prev, bool last) {
+                if (!wave_active) return;
+                const int t0 = t * T::BN;
+                const int kv_valid = min(T::BN, p.Sc - t0);
+                const int lo = max(qc_lo - t0, 0), hi = min(qc_hi - t0, T::BN);
+                wave_step<D, true>(st, pk_prev, deferred, t == 0, last, ks, vs, vs_prev, fa, grp, p.scale_log2,
+                                   kv_valid, lo, hi);
+              });
   if (!wave_active) return;
 
   const float ltot = st.l + __shfl_xor(st.l, 32);
@@ -525,11 +571,15 @@ __global__ __launch_bounds__(Tile<D>::NT, 8 / kBf16Waves) void decode_bf16_kerne
     }
   };
   auto no_hook = [](int, const uint16_t*, const uint16_t*) {};
-  kv_sweep<D>(Kb, Vb, t_begin, t_end, dma, no_hook, [&](int t, const uint16_t* ks, const uint16_t* vs) {
-    if (!wave_active) return;
-    const int kv_valid = min(T::BN, L_kv - t * T::BN);
-    tile_step<D, false>(st, ks, vs, fa, grp, p.scale_log2, kv_valid, 0, 0);
-  });
+  uint32_t pk_prev[16];
+  const bool deferred = wave_group(wave) != 0;
+  kv_sweep<D>(Kb, Vb, t_begin, t_end, dma, no_hook,
+              [&](int t, const uint16_t* ks, const uint16_t* vs, const uint16_t* vs_prev, bool last) {
+                if (!wave_active) return;
+                const int kv_valid = min(T::BN, L_kv - t * T::BN);
+                wave_step<D, false>(st, pk_prev, deferred, t == t_begin, last, ks, vs, vs_prev, fa, grp,
+                                    p.scale_log2, kv_valid, 0, 0);
+              });
   if (!wave_active || rho >= GL) return;
 
   const float ltot = st.l + __shfl_xor(st.l, 32);

@@ -10,19 +10,19 @@ namespace pd {
 constexpr int kDecodeTableRows = 2048;
 
 // bf16 tile engine geometry: waves per workgroup (32 query rows each) and the
-// number of K/V tiles resident in LDS (all but one of them stream in while
-// the oldest is multiplied).  Build-time tunables.
+// number of K/V tiles resident in LDS (the one being multiplied, the previous
+// one, and the rest streaming in).  Build-time tunables.
 #ifndef PD_BF16_WAVES
 #define PD_BF16_WAVES 8
 #endif
 #ifndef PD_BF16_STAGES
-#define PD_BF16_STAGES 3
+#define PD_BF16_STAGES 4
 #endif
 constexpr int kBf16Waves = PD_BF16_WAVES;
 constexpr int kBf16Rows = 32 * kBf16Waves;
 constexpr int kBf16Stages = PD_BF16_STAGES;
 static_assert(kBf16Waves == 4 || kBf16Waves == 8, "4 or 8 waves per workgroup");
-static_assert(kBf16Stages >= 2 && kBf16Stages <= 4, "2 to 4 stages");
+static_assert(kBf16Stages >= 3 && kBf16Stages <= 4, "3 or 4 stages");
 
 // Stage (a).  Element pointers are bf16 bit patterns (uint16_t) or fp32.
 struct PrefillArgs {
