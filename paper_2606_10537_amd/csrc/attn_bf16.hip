@@ -5,9 +5,10 @@
 //   * K/V tiles of 64 rows go from HBM straight into LDS with
 //     global_load_lds_dwordx4 (no register staging), kBf16Stages tiles
 //     resident: the next ones stream in while the oldest is multiplied;
-//   * both tiles are stored row-major with an XOR swizzle of their 16-byte
-//     chunks, so that the K fragment reads (ds_read_b128) and the transposing
-//     V reads (ds_read_b64_tr_b16) are free of bank conflicts;
+//   * both tiles are stored in 64-byte chunk groups with an XOR swizzle
+//     (tile_off), so that the K fragment reads (ds_read_b128) and the
+//     transposing V reads (ds_read_b64_tr_b16) are free of bank conflicts and
+//     every fragment address is a per-lane base plus an immediate offset;
 //   * S^T = K Q^T and O^T += V^T P^T run on v_mfma_f32_32x32x16_bf16 with
 //     fp32 accumulation; Q stays in registers for the whole sweep;
 //   * online softmax in the log2 domain, lazy rescaling of the running output
@@ -37,27 +38,24 @@ struct Tile {
   static constexpr int NT = 64 * NW;         // threads per workgroup
   static constexpr int S = kBf16Stages;      // resident K/V tiles
   static constexpr int CH = D / 8;           // 16-byte chunks per row
-  static constexpr int RPB = 64 / CH;        // rows per 1 KB DMA block (64 lanes x 16 B)
-  static constexpr int BPW = BN / RPB / NW;  // DMA blocks per wave and tile, for K and for V
+  static constexpr int BPW = CH / NW;        // 1 KB DMA blocks (16 rows x 64 B) per wave and tile, K and V
   static constexpr int KS = D / 16;          // MFMA k-steps along d
   static constexpr int DB = D / 32;          // 32-row blocks of O^T
   static constexpr int TILE = BN * D;        // elements of one K or V tile
   static_assert(BPW >= 1, "unsupported head dim");
 };
 
-// Physical chunk of logical 16-byte chunk c of tile row r.  LDS has 64 banks
-// (256 bytes per bank row); ds_read_b128 serves 16 lanes per pass and
-// ds_read_b64 32 lanes, and a pass is conflict-free when its lanes cover all
-// 256 bytes of a bank row.  K: the 16 lanes of a pass read one logical chunk
-// of 16 consecutive rows, so those rows must land on 16 distinct 16-byte bank
-// groups.  V: the 32 lanes of a transposing read cover 64 bytes (4 chunks) of
-// each of 4 consecutive rows, so those rows must land on 4 distinct 64-byte
-// bank groups.  With d = 128 a row is a whole bank row; with d = 64 two rows
-// share one, which the row bit 0 already separates.
-template <int D>
-__device__ __forceinline__ int k_swz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
-template <int D>
-__device__ __forceinline__ int v_swz(int r) { return D == 128 ? ((r & 3) << 2) : (((r >> 1) & 1) << 2); }
+// LDS layout of a 64-row K or V tile, in elements: logical 16-byte chunk c of
+// row r sits at (c / 4) * 2048 + r * 32 + 8 * ((c % 4) ^ ((r / 4) % 4)), i.e.
+// 64-byte chunk groups of all 64 rows one after the other, with the chunks of
+// a group XOR-swizzled by bits 2-3 of the row.  LDS has 64 banks (256 bytes per
+// bank row); ds_read_b128 serves 16 lanes per pass and ds_read_b64 32 lanes,
+// and a pass is conflict-free when its lanes cover a whole bank row.  A K
+// fragment pass reads one chunk of 16 consecutive rows (rows r % 4 and r / 4 %
+// 4 pick 16 distinct 16-byte bank groups); a transposing V pass reads 4 chunks
+// of 4 consecutive rows (again 16 distinct groups).  A 1 KB DMA block is 16
+// rows of one chunk group.
+__device__ __forceinline__ int tile_off(int r, int c) { return (c >> 2) * 2048 + r * 32 + 8 * ((c & 3) ^ ((r >> 2) & 3)); }
 
 // Wave group of a wave (0 or 1): one wave of each group per SIMD.
 #ifndef PD_GROUP_OF_WAVE
@@ -88,24 +86,21 @@ struct WaveState {
   float qmass;  // this lane's partial mass on the query columns (prefill only)
 };
 
-// Lane-constant parts of the LDS fragment addresses (elements).
-template <int D>
+// Lane-constant parts of the LDS fragment addresses (elements).  Everything
+// else (k-step, key block, d block, tile buffer) is an immediate offset.
 struct FragAddr {
-  int k;              // K: row l32 (+ 32 kb), logical chunk 2 ks + grp XOR kx
-  int kx;             // K swizzle of this lane's rows (rows 32 kb + l32 share it)
-  int v[D / 32];      // V transposing read of d block db: key row 4 grp + kq/4 (+ 16 kk + 8 r2)
+  int k[2];   // K fragment, row l32 (+ 32 kb), chunk 2 ks + grp: base for ks % 2, + (ks / 2) * 2048 + kb * 1024
+  int v[2];   // V transposing read: base for r2, + db * 2048 + (16 kk + 8 r2) * 32
   __device__ FragAddr(int lane) {
     const int l32 = lane & 31, grp = lane >> 5;
-    kx = k_swz<D>(l32);
-    k = l32 * D;
-    // Group q = lane / 16 of 16 lanes, kq = lane % 16: this lane points at
-    // V[row][32 db + 16 (q % 2) + 4 (kq % 4)], 4 elements; the swizzle of row
-    // is the same for rows + 16 kk + 8 r2.
-    const int kq = lane & 15, dh = (lane >> 4) & 1;
-    const int row = 4 * grp + (kq >> 2);
-    const int clo = 2 * dh + ((kq & 3) >> 1);
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db) v[db] = row * D + 8 * ((4 * db + clo) ^ v_swz<D>(row)) + 4 * (kq & 1);
+    for (int j = 0; j < 2; ++j) k[j] = tile_off(l32, 2 * j + grp);
+    // Group q = lane / 16 of 16 lanes, kq = lane % 16: this lane points at
+    // V[4 grp + kq/4 + 16 kk + 8 r2][32 db + 16 (q % 2) + 4 (kq % 4)], 4 elements.
+    const int kq = lane & 15, dh = (lane >> 4) & 1;
+    const int row = 4 * grp + (kq >> 2), c = 2 * dh + ((kq & 3) >> 1);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) v[j] = tile_off(row + 8 * j, c) - 8 * 32 * j + 4 * (kq & 1);
   }
 };
 
@@ -118,19 +113,30 @@ struct FragAddr {
 // bf16-rounded weights that multiply V, so rounding P perturbs a convex
 // combination instead of scaling O.
 template <int D>
+__device__ __forceinline__ bf16x8 k_frag(const uint16_t* Ks, const FragAddr& fa, int ks, int kb) {
+  return __builtin_bit_cast(bf16x8, ld16(Ks + fa.k[ks & 1] + (ks >> 1) * 2048 + kb * 1024));
+}
+
+// Fragments are read two k-steps ahead of the MFMAs that use them.
+template <int D>
 __device__ __forceinline__ void s_phase(f32x16 (&s)[2], const WaveState<D>& st, const uint16_t* Ks,
-                                        const FragAddr<D>& fa, int grp) {
+                                        const FragAddr& fa) {
   using T = Tile<D>;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) s[kb] = f32x16{0};
+  bf16x8 a[3][2];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) a[ks][kb] = k_frag<D>(Ks, fa, ks, kb);
 #pragma unroll
   for (int ks = 0; ks < T::KS; ++ks) {
-    const int c = (2 * ks + grp) ^ fa.kx;
+    if (ks + 2 < T::KS) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      bf16x8 a = __builtin_bit_cast(bf16x8, ld16(Ks + 32 * kb * D + fa.k + 8 * c));
-      s[kb] = mfma32x32x16(a, st.qf[ks], s[kb]);
+      for (int kb = 0; kb < 2; ++kb) a[(ks + 2) % 3][kb] = k_frag<D>(Ks, fa, ks + 2, kb);
     }
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) s[kb] = mfma32x32x16(a[ks % 3][kb], st.qf[ks], s[kb]);
   }
 }
 
@@ -206,23 +212,32 @@ __device__ __forceinline__ void softmax_phase(WaveState<D>& st, f32x16 (&s)[2], 
   }
 }
 
+// V^T fragment of k-step kk and d block db (two transposing reads).
+template <int D>
+__device__ __forceinline__ bf16x8 v_frag(const uint16_t* Vs, const FragAddr& fa, int kk, int db) {
+  const uint16_t* vb = Vs + db * 2048 + 16 * kk * 32;
+  const i16x4 lo = ld_tr16(vb + fa.v[0]);
+  const i16x4 hi = ld_tr16(vb + fa.v[1] + 8 * 32);
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
 // P^T operand of k-step kk: keys 16kk + 4grp + {0..3} then 16kk + 8 + 4grp + {0..3}
 // (pk[4kk .. 4kk+3]); the two transposing reads deliver V^T in that order.
+// Fragments are read two MFMAs ahead.
 template <int D>
 __device__ __forceinline__ void pv_phase(WaveState<D>& st, const uint32_t (&pk)[16], const uint16_t* Vs,
-                                         const FragAddr<D>& fa) {
+                                         const FragAddr& fa) {
   using T = Tile<D>;
+  constexpr int N = 4 * T::DB;   // MFMAs: i = kk * DB + db
+  bf16x8 a[3];
+  a[0] = v_frag<D>(Vs, fa, 0, 0);
+  a[1] = v_frag<D>(Vs, fa, 1 / T::DB, 1 % T::DB);
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {
+  for (int i = 0; i < N; ++i) {
+    if (i + 2 < N) a[(i + 2) % 3] = v_frag<D>(Vs, fa, (i + 2) / T::DB, (i + 2) % T::DB);
+    const int kk = i / T::DB, db = i % T::DB;
     const bf16x8 pf = __builtin_bit_cast(bf16x8, u32x4{pk[4 * kk], pk[4 * kk + 1], pk[4 * kk + 2], pk[4 * kk + 3]});
-#pragma unroll
-    for (int db = 0; db < T::DB; ++db) {
-      const uint16_t* vb = Vs + fa.v[db] + 16 * kk * D;
-      const i16x4 lo = ld_tr16(vb);
-      const i16x4 hi = ld_tr16(vb + 8 * D);
-      const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-      st.o[db] = mfma32x32x16(a, pf, st.o[db]);
-    }
+    st.o[db] = mfma32x32x16(a[i % 3], pf, st.o[db]);
   }
 }
 
@@ -236,11 +251,11 @@ __device__ __forceinline__ void pv_phase(WaveState<D>& st, const uint32_t (&pk)[
 template <int D, bool EXACT>
 __device__ __forceinline__ void wave_step(WaveState<D>& st, uint32_t (&pk)[16], bool deferred, bool first, bool last,
                                           const uint16_t* Ks, const uint16_t* Vs, const uint16_t* Vs_prev,
-                                          const FragAddr<D>& fa, int grp, float scale_log2, int kv_valid, int qlo,
+                                          const FragAddr& fa, int grp, float scale_log2, int kv_valid, int qlo,
                                           int qhi) {
   f32x16 s[2];
   if (deferred && !first) pv_phase<D>(st, pk, Vs_prev, fa);
-  s_phase<D>(s, st, Ks, fa, grp);
+  s_phase<D>(s, st, Ks, fa);
   softmax_phase<D, EXACT>(st, s, pk, grp, scale_log2, kv_valid, qlo, qhi);
   if (!deferred || last) pv_phase<D>(st, pk, Vs, fa);
 }
@@ -287,25 +302,26 @@ struct RowPtr {
   const uint16_t* v;
 };
 
-// Issue this wave's share of the DMA of one K/V tile: BPW blocks of RPB rows
-// each for K and for V.  row(r) returns the global K and V pointers of tile row
-// r (already clamped to a valid row); lane takes physical chunk lane % CH of
-// row r = block*RPB + lane / CH and loads the logical chunk that the swizzle
-// places there.  All row pointers are formed before the first DMA is issued:
-// an LDS read (a row table) after a DMA would make the compiler wait for it.
+// Issue this wave's share of the DMA of one K/V tile: BPW blocks for K and
+// for V.  Block b holds rows 16 (b % 4) .. +15 of chunk group b / 4; lane
+// takes row 16 (b % 4) + lane / 4 and loads the logical chunk that tile_off
+// places in its 16-byte slot.  row(r) returns the global K and V pointers of
+// tile row r (already clamped to a valid row).  All row pointers are formed
+// before the first DMA is issued: an LDS read (a row table) after a DMA would
+// make the compiler wait for it.
 template <int D, class Row>
 __device__ __forceinline__ void dma_tile(uint16_t* Kd, uint16_t* Vd, int wave, int lane, Row&& row) {
   using T = Tile<D>;
-  const int pc = lane % T::CH;
   RowPtr rp[T::BPW];
 #pragma unroll
-  for (int j = 0; j < T::BPW; ++j) rp[j] = row((wave * T::BPW + j) * T::RPB + lane / T::CH);
+  for (int j = 0; j < T::BPW; ++j) rp[j] = row(((wave * T::BPW + j) & 3) * 16 + (lane >> 2));
 #pragma unroll
   for (int j = 0; j < T::BPW; ++j) {
     const int blk = wave * T::BPW + j;
-    const int r = blk * T::RPB + lane / T::CH;
-    dma16(rp[j].k + 8 * (pc ^ k_swz<D>(r)), Kd + blk * 512);
-    dma16(rp[j].v + 8 * (pc ^ v_swz<D>(r)), Vd + blk * 512);
+    const int r = (blk & 3) * 16 + (lane >> 2);
+    const int c = 4 * (blk >> 2) + ((lane & 3) ^ ((r >> 2) & 3));
+    dma16(rp[j].k + 8 * c, Kd + blk * 512);
+    dma16(rp[j].v + 8 * c, Vd + blk * 512);
   }
 }
 
@@ -399,7 +415,7 @@ __global__ __launch_bounds__(Tile<D>::NT, 8 / kBf16Waves) void prefill_bf16_kern
       st.qf[ks] = src ? __builtin_bit_cast(bf16x8, ld16(src + 16 * ks + 8 * grp)) : bf16x8{0};
   }
   wave_init(st);
-  const FragAddr<D> fa(lane);
+  const FragAddr fa(lane);
 
   // Row r of the chunk sequence lives at base + r*HD (HD = H_kv*d elements), with
   // base the chunk's rows for r <= C and the shared query/pseudo-label rows after.
@@ -432,8 +448,8 @@ __global__ __launch_bounds__(Tile<D>::NT, 8 / kBf16Waves) void prefill_bf16_kern
       const int r = u / T::CH, c = u % T::CH;
       const int row = t * T::BN + r;
       if (row < C1) {
-        st16(p.k_cache + (base + row) * D + 8 * c, ld16(Ks + r * D + 8 * (c ^ k_swz<D>(r))));
-        st16(p.v_cache + (base + row) * D + 8 * c, ld16(Vs + r * D + 8 * (c ^ v_swz<D>(r))));
+        st16(p.k_cache + (base + row) * D + 8 * c, ld16(Ks + tile_off(r, c)));
+        st16(p.v_cache + (base + row) * D + 8 * c, ld16(Vs + tile_off(r, c)));
       }
     }
   };
@@ -509,7 +525,7 @@ __global__ __launch_bounds__(Tile<D>::NT, 8 / kBf16Waves) void decode_bf16_kerne
       st.qf[ks] = src ? __builtin_bit_cast(bf16x8, ld16(src + 16 * ks + 8 * grp)) : bf16x8{0};
   }
   wave_init(st);
-  const FragAddr<D> fa(lane);
+  const FragAddr fa(lane);
 
   // This shard's tiles.
   const int n_kvt = (L_kv + T::BN - 1) / T::BN;
