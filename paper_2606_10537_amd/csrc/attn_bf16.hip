@@ -33,6 +33,7 @@ typedef short i16x8 __attribute__((ext_vector_type(8)));
 template <int D>
 struct Tile {
   static constexpr int NW = kBf16Waves;      // waves per workgroup
+  static constexpr int NH = kBf16RowsPerWave / 32;   // 32-row groups per wave
   static constexpr int BM = kBf16Rows;       // query rows per workgroup
   static constexpr int BN = 64;              // key rows per KV tile
   static constexpr int NT = 64 * NW;         // threads per workgroup
@@ -61,7 +62,9 @@ __device__ __forceinline__ int tile_off(int r, int c) { return (c >> 2) * 2048 +
 #ifndef PD_GROUP_OF_WAVE
 #define PD_GROUP_OF_WAVE(w) ((w) >> 2)
 #endif
-__device__ __forceinline__ int wave_group(int wave) { return kBf16Waves == 8 ? PD_GROUP_OF_WAVE(wave) : 0; }
+__device__ __forceinline__ int wave_group(int wave) {
+  return (kBf16Waves == 8 && kBf16RowsPerWave == 32) ? PD_GROUP_OF_WAVE(wave) : 0;
+}
 
 __device__ __forceinline__ u32x4 ld16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ void st16(uint16_t* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
@@ -75,7 +78,7 @@ __device__ __forceinline__ void dma16(const uint16_t* g, uint16_t* lds) {
   __builtin_amdgcn_global_load_lds(g, (PD_LDS void*)(lds), 16, 0, 0);
 }
 
-// Engine state of one wave: 32 query rows.
+// Engine state of 32 query rows of a wave (a wave holds NH of them).
 template <int D>
 struct WaveState {
   bf16x8 qf[Tile<D>::KS];
@@ -117,13 +120,16 @@ __device__ __forceinline__ bf16x8 k_frag(const uint16_t* Ks, const FragAddr& fa,
   return __builtin_bit_cast(bf16x8, ld16(Ks + fa.k[ks & 1] + (ks >> 1) * 2048 + kb * 1024));
 }
 
-// Fragments are read two k-steps ahead of the MFMAs that use them.
-template <int D>
-__device__ __forceinline__ void s_phase(f32x16 (&s)[2], const WaveState<D>& st, const uint16_t* Ks,
+// Fragments are read two k-steps ahead of the MFMAs that use them; each K
+// fragment serves the NH row groups of the wave.
+template <int D, int NH>
+__device__ __forceinline__ void s_phase(f32x16 (&s)[NH][2], const WaveState<D> (&st)[NH], const uint16_t* Ks,
                                         const FragAddr& fa) {
   using T = Tile<D>;
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb) s[kb] = f32x16{0};
+  for (int h = 0; h < NH; ++h)
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) s[h][kb] = f32x16{0};
   bf16x8 a[3][2];
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks)
@@ -136,17 +142,27 @@ __device__ __forceinline__ void s_phase(f32x16 (&s)[2], const WaveState<D>& st, 
       for (int kb = 0; kb < 2; ++kb) a[(ks + 2) % 3][kb] = k_frag<D>(Ks, fa, ks + 2, kb);
     }
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) s[kb] = mfma32x32x16(a[ks % 3][kb], st.qf[ks], s[kb]);
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int h = 0; h < NH; ++h) s[h][kb] = mfma32x32x16(a[ks % 3][kb], st[h].qf[ks], s[h][kb]);
   }
 }
 
+// Max of this lane's value and the value of lane l ^ 32 (v_permlane32_swap
+// exchanges the two halves of the wave without going through LDS).
+__device__ __forceinline__ float max_across_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// Softmax of one 32-row group, part 1: mask, row max, lazy rescale of the
+// running output.  Returns -m (log2 domain) for the exponent FMA.  Key of
+// s[kb][r]: 32*kb + 8*(r/4) + 4*grp + r%4.  The max is taken on raw scores (the
+// scale is positive) and the scale is folded into one FMA: p = exp2(s * scale_log2 - m).
 template <int D, bool EXACT>
-__device__ __forceinline__ void softmax_phase(WaveState<D>& st, f32x16 (&s)[2], uint32_t (&pk)[16], int grp,
-                                              float scale_log2, int kv_valid, int qlo, int qhi) {
+__device__ __forceinline__ float softmax_max(WaveState<D>& st, f32x16 (&s)[2], int grp, float scale_log2,
+                                             int kv_valid) {
   using T = Tile<D>;
-  // Key of s[kb][r]: 32*kb + 8*(r/4) + 4*grp + r%4.  The max is taken on raw
-  // scores (the scale is positive) and the scale is folded into one FMA:
-  // p = exp2(s * scale_log2 - m).
   if (kv_valid < 64) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -163,7 +179,7 @@ __device__ __forceinline__ void softmax_phase(WaveState<D>& st, f32x16 (&s)[2], 
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int r = 0; r < 16; r += 2) mx = fmaxf(fmaxf(mx, s[kb][r]), s[kb][r + 1]);
-  mx = fmaxf(mx, __shfl_xor(mx, 32)) * scale_log2;
+  mx = max_across_halves(mx) * scale_log2;
   const bool upd = mx > st.m + 8.0f;
   if (__ballot(upd)) {
     const float mnew = upd ? mx : st.m;
@@ -179,7 +195,15 @@ __device__ __forceinline__ void softmax_phase(WaveState<D>& st, f32x16 (&s)[2], 
 #pragma unroll
       for (int r = 0; r < 16; ++r) st.o[db][r] *= alpha;
   }
-  const float nm = -st.m;
+  return -st.m;
+}
+
+// Part 2 (branch-free): weights p, packed to bf16 in pk; s keeps the fp32 p
+// for the query-column mass.  The rounded weights' sum goes into l (one
+// v_dot2c_f32_bf16 with (1, 1) per packed pair), the exact sum into lx.
+template <int D, bool EXACT>
+__device__ __forceinline__ void softmax_exp(WaveState<D>& st, f32x16 (&s)[2], uint32_t (&pk)[16], float nm,
+                                            float scale_log2) {
   float lsum = 0.f;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
@@ -193,13 +217,17 @@ __device__ __forceinline__ void softmax_phase(WaveState<D>& st, f32x16 (&s)[2], 
       pk[8 * kb + r / 2] = __builtin_bit_cast(uint32_t, bf16x2{(__bf16)p0, (__bf16)p1});
     }
   if constexpr (EXACT) st.lx += lsum;
-  // Sum of the rounded weights: one v_dot2c_f32_bf16 with (1, 1) per packed pair.
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
   float lr = st.l;
 #pragma unroll
   for (int i = 0; i < 16; ++i) lr = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[i]), ones, lr, false);
   st.l = lr;
-  if (EXACT && qlo < qhi) {
+}
+
+// Part 3 (prefill only): mass of the keys qlo..qhi-1 (the query columns).
+template <int D>
+__device__ __forceinline__ void softmax_qmass(WaveState<D>& st, const f32x16 (&s)[2], int grp, int qlo, int qhi) {
+  if (qlo < qhi) {
     float qs = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -210,6 +238,14 @@ __device__ __forceinline__ void softmax_phase(WaveState<D>& st, f32x16 (&s)[2], 
       }
     st.qmass += qs;
   }
+}
+
+template <int D, bool EXACT>
+__device__ __forceinline__ void softmax_phase(WaveState<D>& st, f32x16 (&s)[2], uint32_t (&pk)[16], int grp,
+                                              float scale_log2, int kv_valid, int qlo, int qhi) {
+  const float nm = softmax_max<D, EXACT>(st, s, grp, scale_log2, kv_valid);
+  softmax_exp<D, EXACT>(st, s, pk, nm, scale_log2);
+  if constexpr (EXACT) softmax_qmass<D>(st, s, grp, qlo, qhi);
 }
 
 // V^T fragment of k-step kk and d block db (two transposing reads).
@@ -223,12 +259,12 @@ __device__ __forceinline__ bf16x8 v_frag(const uint16_t* Vs, const FragAddr& fa,
 
 // P^T operand of k-step kk: keys 16kk + 4grp + {0..3} then 16kk + 8 + 4grp + {0..3}
 // (pk[4kk .. 4kk+3]); the two transposing reads deliver V^T in that order.
-// Fragments are read two MFMAs ahead.
-template <int D>
-__device__ __forceinline__ void pv_phase(WaveState<D>& st, const uint32_t (&pk)[16], const uint16_t* Vs,
+// Fragments are read two MFMAs ahead; each serves the NH row groups.
+template <int D, int NH>
+__device__ __forceinline__ void pv_phase(WaveState<D> (&st)[NH], const uint32_t (&pk)[NH][16], const uint16_t* Vs,
                                          const FragAddr& fa) {
   using T = Tile<D>;
-  constexpr int N = 4 * T::DB;   // MFMAs: i = kk * DB + db
+  constexpr int N = 4 * T::DB;   // fragments: i = kk * DB + db
   bf16x8 a[3];
   a[0] = v_frag<D>(Vs, fa, 0, 0);
   a[1] = v_frag<D>(Vs, fa, 1 / T::DB, 1 % T::DB);
@@ -236,28 +272,35 @@ __device__ __forceinline__ void pv_phase(WaveState<D>& st, const uint32_t (&pk)[
   for (int i = 0; i < N; ++i) {
     if (i + 2 < N) a[(i + 2) % 3] = v_frag<D>(Vs, fa, (i + 2) / T::DB, (i + 2) % T::DB);
     const int kk = i / T::DB, db = i % T::DB;
-    const bf16x8 pf = __builtin_bit_cast(bf16x8, u32x4{pk[4 * kk], pk[4 * kk + 1], pk[4 * kk + 2], pk[4 * kk + 3]});
-    st.o[db] = mfma32x32x16(a[i % 3], pf, st.o[db]);
+#pragma unroll
+    for (int h = 0; h < NH; ++h) {
+      const bf16x8 pf =
+          __builtin_bit_cast(bf16x8, u32x4{pk[h][4 * kk], pk[h][4 * kk + 1], pk[h][4 * kk + 2], pk[h][4 * kk + 3]});
+      st[h].o[db] = mfma32x32x16(a[i % 3], pf, st[h].o[db]);
+    }
   }
 }
 
-// The tile step of one wave.  The two wave groups of a workgroup (one wave of
-// each per SIMD) run the phases in different orders so that one group's
-// softmax overlaps the other's MFMAs: group 0 does S, softmax, P*V of tile t;
-// group 1 first does the P*V of tile t-1 (its weights are still in pk), then
-// S and softmax of tile t, and the P*V of the last tile right after its
-// softmax.  The order of the online-softmax updates is the same in both
-// groups.  One code path with wave-uniform guards keeps a single pk array.
-template <int D, bool EXACT>
-__device__ __forceinline__ void wave_step(WaveState<D>& st, uint32_t (&pk)[16], bool deferred, bool first, bool last,
-                                          const uint16_t* Ks, const uint16_t* Vs, const uint16_t* Vs_prev,
+// The tile step of one wave.  With one row group per wave (two waves per
+// SIMD), the two wave groups of a workgroup (one wave of each per SIMD) run the
+// phases in different orders so that one group's softmax overlaps the other's
+// MFMAs: group 0 does S, softmax, P*V of tile t; group 1 first does the P*V of
+// tile t-1 (its weights are still in pk), then S and softmax of tile t, and the
+// P*V of the last tile right after its softmax.  The order of the
+// online-softmax updates is the same in both groups.  One code path with
+// wave-uniform guards keeps a single pk array.  With two row groups per wave
+// (one wave per SIMD) each K and V fragment serves both groups.
+template <int D, int NH, bool EXACT>
+__device__ __forceinline__ void wave_step(WaveState<D> (&st)[NH], uint32_t (&pk)[NH][16], bool deferred, bool first,
+                                          bool last, const uint16_t* Ks, const uint16_t* Vs, const uint16_t* Vs_prev,
                                           const FragAddr& fa, int grp, float scale_log2, int kv_valid, int qlo,
                                           int qhi) {
-  f32x16 s[2];
-  if (deferred && !first) pv_phase<D>(st, pk, Vs_prev, fa);
-  s_phase<D>(s, st, Ks, fa);
-  softmax_phase<D, EXACT>(st, s, pk, grp, scale_log2, kv_valid, qlo, qhi);
-  if (!deferred || last) pv_phase<D>(st, pk, Vs, fa);
+  f32x16 s[NH][2];
+  if (deferred && !first) pv_phase<D, NH>(st, pk, Vs_prev, fa);
+  s_phase<D, NH>(s, st, Ks, fa);
+#pragma unroll
+  for (int h = 0; h < NH; ++h) softmax_phase<D, EXACT>(st[h], s[h], pk[h], grp, scale_log2, kv_valid, qlo, qhi);
+  if (!deferred || last) pv_phase<D, NH>(st, pk, Vs, fa);
 }
 
 template <int D>
@@ -380,7 +423,7 @@ __device__ __forceinline__ void kv_sweep(uint16_t* const* Kb, uint16_t* const* V
 // (b, n, kv-head) group), the per-head query-column mass of the content rows
 // and the log2-domain LSE of the query rows.
 template <int D>
-__global__ __launch_bounds__(Tile<D>::NT, 8 / kBf16Waves) void prefill_bf16_kernel(PrefillArgs p) {
+__global__ __launch_bounds__(Tile<D>::NT, 1) void prefill_bf16_kernel(PrefillArgs p) {
   using T = Tile<D>;
   __shared__ __attribute__((aligned(1024))) uint16_t K0[T::TILE], K1[T::TILE], K2[T::TILE], K3[T::TILE];
   __shared__ __attribute__((aligned(1024))) uint16_t V0[T::TILE], V1[T::TILE], V2[T::TILE], V3[T::TILE];
@@ -402,19 +445,20 @@ __global__ __launch_bounds__(Tile<D>::NT, 8 / kBf16Waves) void prefill_bf16_kern
   const size_t chunk = (size_t)b * p.N + n;
   const size_t qm_base = (p.qm_per_chunk ? chunk : (size_t)b) * (size_t)(p.Lq + p.Lm);
 
-  // Q fragment of this lane's query row.
-  WaveState<D> st;
-  const int qrow = qt * T::BM + wave * 32 + l32;
-  const bool wave_active = qt * T::BM + wave * 32 < p.Sc;
-  {
+  // Q fragments of this lane's query rows (one per row group j).
+  WaveState<D> st[T::NH];
+  const bool wave_active = qt * T::BM + wave * T::NH * 32 < p.Sc;
+#pragma unroll
+  for (int j = 0; j < T::NH; ++j) {
+    const int qrow = qt * T::BM + (wave * T::NH + j) * 32 + l32;
     const uint16_t* src = nullptr;
     if (qrow < C1) src = p.q_pre + ((chunk * C1 + qrow) * p.Hq + h) * D;
     else if (qrow < p.Sc) src = p.q_qm + ((qm_base + (qrow - C1)) * p.Hq + h) * D;
 #pragma unroll
     for (int ks = 0; ks < T::KS; ++ks)
-      st.qf[ks] = src ? __builtin_bit_cast(bf16x8, ld16(src + 16 * ks + 8 * grp)) : bf16x8{0};
+      st[j].qf[ks] = src ? __builtin_bit_cast(bf16x8, ld16(src + 16 * ks + 8 * grp)) : bf16x8{0};
+    wave_init(st[j]);
   }
-  wave_init(st);
   const FragAddr fa(lane);
 
   // Row r of the chunk sequence lives at base + r*HD (HD = H_kv*d elements), with
@@ -455,7 +499,7 @@ __global__ __launch_bounds__(Tile<D>::NT, 8 / kBf16Waves) void prefill_bf16_kern
   };
 
   const int qc_lo = C1, qc_hi = C1 + p.Lq;   // query columns counted by Eq. 5
-  uint32_t pk_prev[16];
+  uint32_t pk_prev[T::NH][16];
   const bool deferred = wave_group(wave) != 0;
   kv_sweep<D>(Kb, Vb, 0, p.n_kvt, dma, cache_write,
               [&](int t, const uint16_t* ks, const uint16_t* vs, const uint16_t* vs_prev, bool last) {
@@ -463,23 +507,27 @@ __global__ __launch_bounds__(Tile<D>::NT, 8 / kBf16Waves) void prefill_bf16_kern
                 const int t0 = t * T::BN;
                 const int kv_valid = min(T::BN, p.Sc - t0);
                 const int lo = max(qc_lo - t0, 0), hi = min(qc_hi - t0, T::BN);
-                wave_step<D, true>(st, pk_prev, deferred, t == 0, last, ks, vs, vs_prev, fa, grp, p.scale_log2,
-                                   kv_valid, lo, hi);
+                wave_step<D, T::NH, true>(st, pk_prev, deferred, t == 0, last, ks, vs, vs_prev, fa, grp,
+                                          p.scale_log2, kv_valid, lo, hi);
               });
   if (!wave_active) return;
 
-  const float ltot = st.l + __shfl_xor(st.l, 32);
-  const float lxtot = st.lx + __shfl_xor(st.lx, 32);
-  const float qtot = st.qmass + __shfl_xor(st.qmass, 32);
-  const float inv = 1.0f / ltot;
-  if (qrow < p.Sc) {
-    const size_t orow = ((chunk * p.Sc + qrow) * p.Hq + h) * D;
-    if (p.out_f32) store_row_f32<D>(reinterpret_cast<float*>(p.o) + orow, st, inv, grp);
-    else store_row_bf16<D>(p.o + orow, st, inv, grp);
-    if (grp == 0) {
-      const size_t hb = chunk * p.Hq + h;
-      if (qrow >= 1 && qrow < C1) p.part_i[hb * p.C + (qrow - 1)] = qtot / lxtot;
-      if (qrow >= qc_lo && qrow < qc_hi) p.lse_q[hb * p.Lq + (qrow - qc_lo)] = st.m + __log2f(lxtot);
+#pragma unroll
+  for (int j = 0; j < T::NH; ++j) {
+    const int qrow = qt * T::BM + (wave * T::NH + j) * 32 + l32;
+    const float ltot = st[j].l + __shfl_xor(st[j].l, 32);
+    const float lxtot = st[j].lx + __shfl_xor(st[j].lx, 32);
+    const float qtot = st[j].qmass + __shfl_xor(st[j].qmass, 32);
+    const float inv = 1.0f / ltot;
+    if (qrow < p.Sc) {
+      const size_t orow = ((chunk * p.Sc + qrow) * p.Hq + h) * D;
+      if (p.out_f32) store_row_f32<D>(reinterpret_cast<float*>(p.o) + orow, st[j], inv, grp);
+      else store_row_bf16<D>(p.o + orow, st[j], inv, grp);
+      if (grp == 0) {
+        const size_t hb = chunk * p.Hq + h;
+        if (qrow >= 1 && qrow < C1) p.part_i[hb * p.C + (qrow - 1)] = qtot / lxtot;
+        if (qrow >= qc_lo && qrow < qc_hi) p.lse_q[hb * p.Lq + (qrow - qc_lo)] = st[j].m + __log2f(lxtot);
+      }
     }
   }
 }
@@ -490,7 +538,7 @@ __global__ __launch_bounds__(Tile<D>::NT, 8 / kBf16Waves) void prefill_bf16_kern
 // is head g*G + rho / L_d, decode row rho % L_d.  KV row j of the shard walks:
 // [kept chunks: BOS + kept slots] ; [static rows] ; [own rows].
 template <int D>
-__global__ __launch_bounds__(Tile<D>::NT, 8 / kBf16Waves) void decode_bf16_kernel(DecodeArgs p) {
+__global__ __launch_bounds__(Tile<D>::NT, 1) void decode_bf16_kernel(DecodeArgs p) {
   using T = Tile<D>;
   __shared__ __attribute__((aligned(1024))) uint16_t K0[T::TILE], K1[T::TILE], K2[T::TILE], K3[T::TILE];
   __shared__ __attribute__((aligned(1024))) uint16_t V0[T::TILE], V1[T::TILE], V2[T::TILE], V3[T::TILE];
@@ -513,18 +561,19 @@ __global__ __launch_bounds__(Tile<D>::NT, 8 / kBf16Waves) void decode_bf16_kerne
   const int n_sel = p.K * (1 + p.Bt);
   const int L_kv = n_sel + p.n_static + p.Ld;
 
-  WaveState<D> st;
-  const int rho = qt * T::BM + wave * 32 + l32;
-  const bool wave_active = qt * T::BM + wave * 32 < GL;
-  const int hq = g * p.G + (rho < GL ? rho / p.Ld : 0);
-  const int rr = rho < GL ? rho % p.Ld : 0;
-  {
+  WaveState<D> st[T::NH];
+  const bool wave_active = qt * T::BM + wave * T::NH * 32 < GL;
+#pragma unroll
+  for (int j = 0; j < T::NH; ++j) {
+    const int rho = qt * T::BM + (wave * T::NH + j) * 32 + l32;
+    const int hq = g * p.G + (rho < GL ? rho / p.Ld : 0);
+    const int rr = rho < GL ? rho % p.Ld : 0;
     const uint16_t* src = rho < GL ? p.q_dec + (((size_t)b * p.Ld + rr) * p.Hq + hq) * D : nullptr;
 #pragma unroll
     for (int ks = 0; ks < T::KS; ++ks)
-      st.qf[ks] = src ? __builtin_bit_cast(bf16x8, ld16(src + 16 * ks + 8 * grp)) : bf16x8{0};
+      st[j].qf[ks] = src ? __builtin_bit_cast(bf16x8, ld16(src + 16 * ks + 8 * grp)) : bf16x8{0};
+    wave_init(st[j]);
   }
-  wave_init(st);
   const FragAddr fa(lane);
 
   // This shard's tiles.
@@ -587,29 +636,36 @@ __global__ __launch_bounds__(Tile<D>::NT, 8 / kBf16Waves) void decode_bf16_kerne
     }
   };
   auto no_hook = [](int, const uint16_t*, const uint16_t*) {};
-  uint32_t pk_prev[16];
+  uint32_t pk_prev[T::NH][16];
   const bool deferred = wave_group(wave) != 0;
   kv_sweep<D>(Kb, Vb, t_begin, t_end, dma, no_hook,
               [&](int t, const uint16_t* ks, const uint16_t* vs, const uint16_t* vs_prev, bool last) {
                 if (!wave_active) return;
                 const int kv_valid = min(T::BN, L_kv - t * T::BN);
-                wave_step<D, false>(st, pk_prev, deferred, t == t_begin, last, ks, vs, vs_prev, fa, grp,
-                                    p.scale_log2, kv_valid, 0, 0);
+                wave_step<D, T::NH, false>(st, pk_prev, deferred, t == t_begin, last, ks, vs, vs_prev, fa, grp,
+                                           p.scale_log2, kv_valid, 0, 0);
               });
-  if (!wave_active || rho >= GL) return;
+  if (!wave_active) return;
 
-  const float ltot = st.l + __shfl_xor(st.l, 32);
-  const float inv = 1.0f / ltot;
-  const float lse2 = st.m + __log2f(ltot);
-  if (p.S == 1) {
-    const size_t orow = (((size_t)b * p.Ld + rr) * p.Hq + hq) * D;
-    if (p.out_f32) store_row_f32<D>(reinterpret_cast<float*>(p.o_dec) + orow, st, inv, grp);
-    else store_row_bf16<D>(reinterpret_cast<uint16_t*>(p.o_dec) + orow, st, inv, grp);
-    if (p.lse_dec && grp == 0) p.lse_dec[((size_t)b * p.Hq + hq) * p.Ld + rr] = lse2 * kLn2;
-  } else {
-    const size_t row = (((size_t)sp * p.B + b) * p.Hq + hq) * p.Ld + rr;
-    store_row_f32<D>(p.o_part + row * D, st, inv, grp);
-    if (grp == 0) p.lse_part[row] = lse2;
+#pragma unroll
+  for (int j = 0; j < T::NH; ++j) {
+    const int rho = qt * T::BM + (wave * T::NH + j) * 32 + l32;
+    if (rho >= GL) continue;
+    const int hq = g * p.G + rho / p.Ld;
+    const int rr = rho % p.Ld;
+    const float ltot = st[j].l + __shfl_xor(st[j].l, 32);
+    const float inv = 1.0f / ltot;
+    const float lse2 = st[j].m + __log2f(ltot);
+    if (p.S == 1) {
+      const size_t orow = (((size_t)b * p.Ld + rr) * p.Hq + hq) * D;
+      if (p.out_f32) store_row_f32<D>(reinterpret_cast<float*>(p.o_dec) + orow, st[j], inv, grp);
+      else store_row_bf16<D>(reinterpret_cast<uint16_t*>(p.o_dec) + orow, st[j], inv, grp);
+      if (p.lse_dec && grp == 0) p.lse_dec[((size_t)b * p.Hq + hq) * p.Ld + rr] = lse2 * kLn2;
+    } else {
+      const size_t row = (((size_t)sp * p.B + b) * p.Hq + hq) * p.Ld + rr;
+      store_row_f32<D>(p.o_part + row * D, st[j], inv, grp);
+      if (grp == 0) p.lse_part[row] = lse2;
+    }
   }
 }
 

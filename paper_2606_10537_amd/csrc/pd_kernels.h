@@ -9,17 +9,22 @@ namespace pd {
 // LDS table; the host raises the shard count until every shard fits.
 constexpr int kDecodeTableRows = 2048;
 
-// bf16 tile engine geometry: waves per workgroup (32 query rows each) and the
-// number of K/V tiles resident in LDS (the one being multiplied, the previous
+// bf16 tile engine geometry: query rows per wave (32 or 64), waves per
+// workgroup and the number of K/V tiles resident in LDS (the one being multiplied, the previous
 // one, and the rest streaming in).  Build-time tunables.
+#ifndef PD_BF16_ROWS_PER_WAVE
+#define PD_BF16_ROWS_PER_WAVE 32
+#endif
 #ifndef PD_BF16_WAVES
-#define PD_BF16_WAVES 8
+#define PD_BF16_WAVES (PD_BF16_ROWS_PER_WAVE == 32 ? 8 : 4)
 #endif
 #ifndef PD_BF16_STAGES
 #define PD_BF16_STAGES 4
 #endif
+constexpr int kBf16RowsPerWave = PD_BF16_ROWS_PER_WAVE;
 constexpr int kBf16Waves = PD_BF16_WAVES;
-constexpr int kBf16Rows = 32 * kBf16Waves;
+constexpr int kBf16Rows = kBf16RowsPerWave * kBf16Waves;
+static_assert(kBf16RowsPerWave == 32 || kBf16RowsPerWave == 64, "32 or 64 query rows per wave");
 constexpr int kBf16Stages = PD_BF16_STAGES;
 static_assert(kBf16Waves == 4 || kBf16Waves == 8, "4 or 8 waves per workgroup");
 static_assert(kBf16Stages >= 3 && kBf16Stages <= 4, "3 or 4 stages");
