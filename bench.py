@@ -35,6 +35,11 @@ def parse():
     p.add_argument("--dec-pool", type=int, default=4, help="decode input slots per layer")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU time budget of the oracle sample")
+    p.add_argument("--flush-mib", type=int, default=0,
+                   help="write this many MiB before every decode launch, so that each launch starts with the "
+                        "last-level cache (MALL) holding none of its operands (cold numbers)")
+    p.add_argument("--no-achievable", action="store_true",
+                   help="skip the achievable-peak measurements (library GEMM, device copy) after the timed region")
     p.add_argument("--calib-copy-mib", type=int, default=0,
                    help="before timing, copy this many MiB once (a plain copy kernel of known size for "
                         "calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -135,6 +140,36 @@ def cpu_baseline(w, budget_s):
     }
 
 
+def achievable_peaks(torch, dev):
+    """Achievable (not published) peaks on this GPU, measured after the timed region: the library's
+    MFMA-rate diagnostic (register-only v_mfma_f32_32x32x16_bf16 chains on every CU) and a
+    device-to-device copy of 4 GiB (read + write bytes)."""
+    from paper_2606_10537_amd import _lib
+    n_wg, iters = 2048, 4000
+    sink = torch.empty(n_wg * 256, dtype=torch.float32, device=dev)
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    _lib.pd_mfma_rate_probe(n_wg, iters, sink)
+    s.record()
+    for _ in range(3):
+        _lib.pd_mfma_rate_probe(n_wg, iters, sink)
+    e.record()
+    torch.cuda.synchronize()
+    mfma = 3.0 * n_wg * 4 * iters * 8 * 32768 / (s.elapsed_time(e) * 1e-3) / 1e12
+    src = torch.empty(4 << 30, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    s.record()
+    for _ in range(5):
+        dst.copy_(src)
+    e.record()
+    torch.cuda.synchronize()
+    copy = 2.0 * src.numel() * 5 / (s.elapsed_time(e) * 1e-3) / 1e9
+    del src, dst
+    return {"mfma_tflops": round(mfma, 1), "hbm_gbps": round(copy, 1),
+            "method": "pd_mfma_rate_probe (2048 workgroups x 4 waves x 4 independent 32x32x16 bf16 chains) "
+                      "and a 4 GiB device copy (read + write bytes)"}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -176,6 +211,7 @@ def main():
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
 
+    flush = torch.empty(args.flush_mib << 20, dtype=torch.uint8, device=dev) if args.flush_mib else None
     n_ev = L * T
     ev_pre = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(L)]
     ev_dec = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_ev)]
@@ -198,6 +234,8 @@ def main():
                 dd = dec_pool[l][t % dec_slots]
                 _lib.pd_score_select(d, K, Bt, dd["q_dec"], key_mean[l], tok_rank[l], chunk_idx, tok_slot, None,
                                      ws_sel, sh)
+                if flush is not None:
+                    flush.fill_(t & 0xFF)
                 if record:
                     ev_dec[i][0].record(stream)
                 _lib.pd_sparse_decode_attn(d, K, Bt, dd["q_dec"], dd["k_dec"], dd["v_dec"], k_cache[l], v_cache[l],
@@ -255,6 +293,7 @@ def main():
                  "launch_ms": round(dec_kern_ms, 5), "flop_per_launch": dec_flop,
                  "bytes_per_launch": dec_bytes})
 
+    traffic = roof.get("traffic")
     res = {
         "metric": "denoising steps/sec + decode-attn HBM GB/s + prefill MFMA TFLOP/s at 32K",
         "value": round(T / (ms * 1e-3), 3),
@@ -275,9 +314,19 @@ def main():
         "prefill_ms_per_layer": round(pre_ms_layer, 3),
         "prefill_tflops": round(pre_tflops, 2),
         "prefill_mfma_frac": round(pre_tflops / PEAK_BF16_TFLOPS, 4),
+        "decode_dram_gbps": round(traffic / (dec_kern_ms * 1e-3) / 1e9, 1) if traffic else None,
+        "decode_binding_roof_frac": round(max(dec_flop / (PEAK_BF16_TFLOPS * 1e12), dec_bytes / (PEAK_HBM_GBPS * 1e9))
+                                          / (dec_kern_ms * 1e-3), 4),
+        "cold_flush_mib": args.flush_mib,
         "roofline": roof,
         "wall_s": round(wall, 3),
     }
+    if not args.no_achievable:
+        ach = achievable_peaks(torch, dev)
+        res["achievable"] = ach
+        roof["frac_of_achievable"] = round(roof["achieved"] / (ach["mfma_tflops"] if roof["bound"] == "mfma"
+                                                               else ach["hbm_gbps"]), 4)
+        res["prefill_frac_of_achievable"] = round(pre_tflops / ach["mfma_tflops"], 4)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)

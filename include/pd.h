@@ -178,6 +178,17 @@ size_t pd_workspace_bytes(const pd_dims *dims, int32_t top_k, int32_t tok_budget
 int32_t pd_decode_splits(const pd_dims *dims, int32_t top_k, int32_t tok_budget,
                          int32_t n_static, int32_t num_splits);
 
+/* Diagnostic: the device's achievable dense bf16 MFMA rate, the yardstick the
+ * attention kernels are compared with besides the published peak.
+ * Launches n_workgroups (1..2^20) workgroups of 4 waves; each wave runs iters
+ * iterations of 8 v_mfma_f32_32x32x16_bf16 (32768 FLOP each) on register
+ * operands, so one call performs n_workgroups * 4 * iters * 8 * 32768 FLOP.
+ * sink: caller-owned device buffer of n_workgroups * 256 floats (16-B aligned)
+ * that receives one value per thread.  Asynchronous on stream; time it with
+ * events.  Errors: PD_ERR_NULL_PTR, PD_ERR_BAD_DIMS, PD_ERR_MISALIGNED,
+ * PD_ERR_HIP. */
+pd_status pd_mfma_rate_probe(int32_t n_workgroups, int32_t iters, float *sink, void *stream);
+
 const char *pd_status_string(pd_status s);
 const char *pd_last_error_message(void); /* thread-local detail of the last error */
 const char *pd_version(void);

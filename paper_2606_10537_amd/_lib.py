@@ -19,7 +19,7 @@ STATUS = {0: "PD_OK", 1: "PD_ERR_NULL_PTR", 2: "PD_ERR_BAD_DIMS", 3: "PD_ERR_UNS
 
 EXPORTS = ["pd_prefill_chunks", "pd_score_select", "pd_sparse_decode_attn", "pd_cache_bytes",
            "pd_workspace_bytes", "pd_decode_splits", "pd_status_string", "pd_last_error_message",
-           "pd_version"]
+           "pd_version", "pd_mfma_rate_probe"]
 
 
 class PdError(RuntimeError):
@@ -99,6 +99,8 @@ def load(path: str = LIB_PATH):
     lib.pd_status_string.restype = ctypes.c_char_p
     lib.pd_last_error_message.argtypes = []
     lib.pd_last_error_message.restype = ctypes.c_char_p
+    lib.pd_mfma_rate_probe.argtypes = [i32, i32, vp, vp]
+    lib.pd_mfma_rate_probe.restype = ctypes.c_int
     lib.pd_version.argtypes = []
     lib.pd_version.restype = ctypes.c_char_p
     _lib = lib
@@ -171,3 +173,8 @@ def pd_sparse_decode_attn(dims: Dims, top_k, tok_budget, q_dec, k_dec, v_dec, k_
         _ptr(k_cache), _ptr(v_cache), _ptr(chunk_idx), _ptr(tok_slot), _ptr(k_static), _ptr(v_static),
         n_static, _ptr(o_dec), _ptr(lse_dec), num_splits, _ptr(workspace), _nbytes(workspace),
         _stream(stream)))
+
+
+def pd_mfma_rate_probe(n_workgroups, iters, sink, stream=None):
+    """Launch the MFMA-rate diagnostic (n_workgroups * 4 * iters * 8 * 32768 FLOP)."""
+    _check(load().pd_mfma_rate_probe(n_workgroups, iters, _ptr(sink), _stream(stream)))

@@ -14,7 +14,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libpd.so")
-SOURCES = ["pd_api.hip", "attn_bf16.hip", "attn_f32.hip", "select.hip"]
+SOURCES = ["pd_api.hip", "attn_bf16.hip", "attn_f32.hip", "select.hip", "diag.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

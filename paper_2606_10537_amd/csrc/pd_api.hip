@@ -175,6 +175,14 @@ extern "C" {
 
 const char* pd_version(void) { return "pd-mi355x 0.1 (gfx950)"; }
 
+pd_status pd_mfma_rate_probe(int32_t n_workgroups, int32_t iters, float* sink, void* stream) {
+  if (!sink) return fail(PD_ERR_NULL_PTR, "sink is NULL");
+  if (n_workgroups < 1 || iters < 1 || n_workgroups > (1 << 20))
+    return fail(PD_ERR_BAD_DIMS, "n_workgroups=%d must be in 1..2^20 and iters=%d >= 1", n_workgroups, iters);
+  if (!aligned16(sink)) return fail(PD_ERR_MISALIGNED, "sink is not 16-byte aligned");
+  return hip_status(pd::launch_mfma_rate(n_workgroups, iters, sink, (hipStream_t)stream), "mfma rate probe");
+}
+
 const char* pd_status_string(pd_status s) {
   switch (s) {
     case PD_OK: return "PD_OK";

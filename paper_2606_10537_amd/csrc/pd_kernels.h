@@ -94,6 +94,7 @@ struct SelectArgs {
   float scale;
 };
 hipError_t launch_score_select(const SelectArgs& a, hipStream_t s);
+hipError_t launch_mfma_rate(int n_workgroups, int iters, float* sink, hipStream_t s);
 hipError_t launch_token_rank(const float* tok_score, int32_t* tok_rank, int B, int N, int C, hipStream_t s);
 int select_row_splits(int Ld);
 

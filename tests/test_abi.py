@@ -119,6 +119,13 @@ def test_decode_validation(lib):
     assert call(splits=4, w=None) == 5
 
 
+def test_mfma_probe_validation(lib):
+    assert lib.pd_mfma_rate_probe(0, 10, A, None) == 2
+    assert lib.pd_mfma_rate_probe(4, 0, A, None) == 2
+    assert lib.pd_mfma_rate_probe(4, 10, None, None) == 1
+    assert lib.pd_mfma_rate_probe(4, 10, MIS, None) == 4
+
+
 def test_size_queries():
     d = dims(batch=2, n_chunks=3, chunk_len=100, n_heads_kv=2, n_heads_q=4, head_dim=128, dtype=PD_BF16)
     assert _lib.pd_cache_bytes(d) == 2 * 3 * 2 * 101 * 128 * 2
