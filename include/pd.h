@@ -165,6 +165,48 @@ pd_status pd_sparse_decode_attn(const pd_dims *dims, int32_t top_k, int32_t tok_
                                 void *o_dec, float *lse_dec, int32_t num_splits,
                                 void *workspace, size_t ws_bytes, void *stream);
 
+/*
+ * Static-selection mode (the paper selects once, before the denoising loop:
+ * Section 5.2 selection from the pseudo-label rows, reused for every step of
+ * Section 5.3).  Three calls per layer replace the per-step pd_score_select +
+ * gathered decode:
+ *
+ * pd_score_select_static: as pd_score_select, but the mean query is taken
+ *   over the L_m pseudo-label rows of q_qm (rows L_q..L_q+L_m-1 of each
+ *   sequence's q/m block, in the layout dims->qm_per_chunk gives; chunk 0's
+ *   copy when per chunk) instead of the decode rows.  Needs m_len >= 1.
+ *   workspace: >= pd_workspace_bytes(dims, top_k, tok_budget, 0, 1) bytes.
+ *
+ * pd_gather_selected: copies, once, the prefix rows a decode step reads into
+ *   contiguous buffers k_sel, v_sel [B][H_kv][top_k*(1+tok_budget)][d]
+ *   (dims->dtype): for each kept chunk chunk_idx[b][k] in order, its BOS row
+ *   (slot 0) and then the rows at slots tok_slot[b][k][*].  Bit-exact copies;
+ *   no workspace.
+ *
+ * pd_sparse_decode_attn_compact: pd_sparse_decode_attn whose prefix rows are
+ *   rows 0..n_sel-1 of k_sel, v_sel [B][H_kv][n_sel][d] instead of rows
+ *   gathered from the chunk cache (0 <= n_sel <= 2^20; k_sel/v_sel may be
+ *   NULL when n_sel = 0).  With the buffers of pd_gather_selected and
+ *   n_sel = top_k*(1+tok_budget) the result is that of pd_sparse_decode_attn
+ *   with the same selection.  workspace: >= pd_compact_workspace_bytes bytes.
+ * Errors as for the per-step calls.
+ */
+pd_status pd_score_select_static(const pd_dims *dims, int32_t top_k, int32_t tok_budget,
+                                 const void *q_qm, const float *key_mean, const int32_t *tok_rank,
+                                 int32_t *chunk_idx, int32_t *tok_slot, float *chunk_score,
+                                 void *workspace, size_t ws_bytes, void *stream);
+pd_status pd_gather_selected(const pd_dims *dims, int32_t top_k, int32_t tok_budget,
+                             const void *k_cache, const void *v_cache,
+                             const int32_t *chunk_idx, const int32_t *tok_slot,
+                             void *k_sel, void *v_sel, void *stream);
+pd_status pd_sparse_decode_attn_compact(const pd_dims *dims, int32_t n_sel,
+                                        const void *q_dec, const void *k_dec, const void *v_dec,
+                                        const void *k_sel, const void *v_sel,
+                                        const void *k_static, const void *v_static, int32_t n_static,
+                                        void *o_dec, float *lse_dec, int32_t num_splits,
+                                        void *workspace, size_t ws_bytes, void *stream);
+size_t pd_compact_workspace_bytes(const pd_dims *dims, int32_t n_sel, int32_t num_splits);
+
 /* Bytes of ONE of k_cache / v_cache for one layer: B*N*H_kv*(1+C)*d*elem. */
 size_t pd_cache_bytes(const pd_dims *dims);
 

@@ -18,6 +18,8 @@ that each step can be checked against the paper by eye:
   kept chunk (Section 5.2, inter- and intra-chunk sparsity).
 * ``decode``   -- stage (c): attention of the decode block over the selected
   prefix KV, the static query KV and its own KV (Section 5.3, prefix reuse).
+* ``static``   -- static-selection mode: selection once from the pseudo-label
+  rows, the kept rows compacted into a contiguous buffer, decode over it.
 
 Parity status of each function is stated in its docstring ("pinned by ...").
 """
@@ -32,6 +34,13 @@ from .prefill import (
 )
 from .select import chunk_scores_ref, topk_ref, score_select_ref, token_rank_ref, tokens_by_rank_ref
 from .decode import decode_kv_rows, decode_unit_ref, decode_ref
+from .static import (
+    pseudo_label_queries,
+    static_select_ref,
+    gather_selected_ref,
+    decode_compact_unit_ref,
+    decode_compact_ref,
+)
 
 __all__ = [
     "chunk_rows",
@@ -48,4 +57,9 @@ __all__ = [
     "decode_kv_rows",
     "decode_unit_ref",
     "decode_ref",
+    "pseudo_label_queries",
+    "static_select_ref",
+    "gather_selected_ref",
+    "decode_compact_unit_ref",
+    "decode_compact_ref",
 ]

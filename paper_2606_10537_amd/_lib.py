@@ -19,7 +19,8 @@ STATUS = {0: "PD_OK", 1: "PD_ERR_NULL_PTR", 2: "PD_ERR_BAD_DIMS", 3: "PD_ERR_UNS
 
 EXPORTS = ["pd_prefill_chunks", "pd_score_select", "pd_sparse_decode_attn", "pd_cache_bytes",
            "pd_workspace_bytes", "pd_decode_splits", "pd_status_string", "pd_last_error_message",
-           "pd_version", "pd_mfma_rate_probe"]
+           "pd_version", "pd_mfma_rate_probe", "pd_score_select_static", "pd_gather_selected",
+           "pd_sparse_decode_attn_compact", "pd_compact_workspace_bytes"]
 
 
 class PdError(RuntimeError):
@@ -99,6 +100,14 @@ def load(path: str = LIB_PATH):
     lib.pd_status_string.restype = ctypes.c_char_p
     lib.pd_last_error_message.argtypes = []
     lib.pd_last_error_message.restype = ctypes.c_char_p
+    lib.pd_score_select_static.argtypes = [dp, i32, i32, vp, fp, fp, vp, vp, fp, vp, sz, vp]
+    lib.pd_score_select_static.restype = ctypes.c_int
+    lib.pd_gather_selected.argtypes = [dp, i32, i32] + [vp] * 6 + [vp]
+    lib.pd_gather_selected.restype = ctypes.c_int
+    lib.pd_sparse_decode_attn_compact.argtypes = [dp, i32] + [vp] * 7 + [i32, vp, fp, i32, vp, sz, vp]
+    lib.pd_sparse_decode_attn_compact.restype = ctypes.c_int
+    lib.pd_compact_workspace_bytes.argtypes = [dp, i32, i32]
+    lib.pd_compact_workspace_bytes.restype = sz
     lib.pd_mfma_rate_probe.argtypes = [i32, i32, vp, vp]
     lib.pd_mfma_rate_probe.restype = ctypes.c_int
     lib.pd_version.argtypes = []
@@ -173,6 +182,36 @@ def pd_sparse_decode_attn(dims: Dims, top_k, tok_budget, q_dec, k_dec, v_dec, k_
         _ptr(k_cache), _ptr(v_cache), _ptr(chunk_idx), _ptr(tok_slot), _ptr(k_static), _ptr(v_static),
         n_static, _ptr(o_dec), _ptr(lse_dec), num_splits, _ptr(workspace), _nbytes(workspace),
         _stream(stream)))
+
+
+def pd_score_select_static(dims: Dims, top_k, tok_budget, q_qm, key_mean, tok_rank, chunk_idx, tok_slot,
+                           chunk_score, workspace, stream=None):
+    """Static-selection mode: selection from the pseudo-label rows of q_qm (see include/pd.h)."""
+    _check(load().pd_score_select_static(
+        ctypes.byref(dims.c()), top_k, tok_budget, _ptr(q_qm), _ptr(key_mean), _ptr(tok_rank),
+        _ptr(chunk_idx), _ptr(tok_slot), _ptr(chunk_score), _ptr(workspace), _nbytes(workspace),
+        _stream(stream)))
+
+
+def pd_gather_selected(dims: Dims, top_k, tok_budget, k_cache, v_cache, chunk_idx, tok_slot, k_sel, v_sel,
+                       stream=None):
+    """Static-selection mode: copy the kept rows into contiguous buffers (see include/pd.h)."""
+    _check(load().pd_gather_selected(
+        ctypes.byref(dims.c()), top_k, tok_budget, _ptr(k_cache), _ptr(v_cache), _ptr(chunk_idx),
+        _ptr(tok_slot), _ptr(k_sel), _ptr(v_sel), _stream(stream)))
+
+
+def pd_sparse_decode_attn_compact(dims: Dims, n_sel, q_dec, k_dec, v_dec, k_sel, v_sel, k_static, v_static,
+                                  n_static, o_dec, lse_dec, num_splits, workspace, stream=None):
+    """Stage (c) over a compact prefix buffer (see include/pd.h)."""
+    _check(load().pd_sparse_decode_attn_compact(
+        ctypes.byref(dims.c()), n_sel, _ptr(q_dec), _ptr(k_dec), _ptr(v_dec), _ptr(k_sel), _ptr(v_sel),
+        _ptr(k_static), _ptr(v_static), n_static, _ptr(o_dec), _ptr(lse_dec), num_splits, _ptr(workspace),
+        _nbytes(workspace), _stream(stream)))
+
+
+def pd_compact_workspace_bytes(dims: Dims, n_sel, num_splits=0) -> int:
+    return load().pd_compact_workspace_bytes(ctypes.byref(dims.c()), n_sel, num_splits)
 
 
 def pd_mfma_rate_probe(n_workgroups, iters, sink, stream=None):

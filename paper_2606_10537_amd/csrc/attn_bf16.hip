@@ -558,7 +558,7 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void decode_bf16_kernel(DecodeArgs 
   const int b = lid / p.Hkv;
   const int GL = p.G * p.Ld;
   const int C1 = p.C + 1;
-  const int n_sel = p.K * (1 + p.Bt);
+  const int n_sel = p.n_sel;
   const int L_kv = n_sel + p.n_static + p.Ld;
 
   WaveState<D> st[T::NH];
@@ -581,12 +581,16 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void decode_bf16_kernel(DecodeArgs 
   const int t_begin = (int)(((long long)n_kvt * sp) / p.S);
   const int t_end = (int)(((long long)n_kvt * (sp + 1)) / p.S);
 
-  const size_t cache_bg = ((size_t)b * p.N * p.Hkv + g) * C1;   // + n*Hkv*C1 + slot
-  // Gathered rows of this shard: row codes into LDS once (the host keeps every
+  // Prefix rows of (b, g): gathered from the chunk cache (row n*Hkv*C1 + slot
+  // from this base), or, in compact mode, row j of the contiguous buffer.
+  const size_t cache_bg = p.compact ? ((size_t)b * p.Hkv + g) * n_sel : ((size_t)b * p.N * p.Hkv + g) * C1;
+  // Prefix rows of this shard: row codes into LDS once (the host keeps every
   // shard within kDecodeTableRows rows), so tile loads need no index fetch.
   const int j_lo = t_begin * T::BN;
   const int j_hi = min(t_end * T::BN, n_sel);
-  {
+  if (p.compact) {
+    for (int j = j_lo + tid; j < j_hi; j += T::NT) rowtab[j - j_lo] = j;
+  } else {
     const int32_t* cidx = p.chunk_idx + (size_t)b * p.K;
     const int32_t* tslot = p.tok_slot + (size_t)b * p.K * p.Bt;
     for (int j = j_lo + tid; j < j_hi; j += T::NT) {

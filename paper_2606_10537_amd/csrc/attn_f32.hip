@@ -219,7 +219,7 @@ __global__ __launch_bounds__(64) void decode_f32_kernel(DecodeArgs p) {
   const int b = lid / p.Hq;
   const int g = h / p.G;
   const int C1 = p.C + 1;
-  const int n_sel = p.K * (1 + p.Bt);
+  const int n_sel = p.n_sel;
   const int L_kv = n_sel + p.n_static + p.Ld;
   const int tid = threadIdx.x;
   const int r = rb * kF32Rows + tid;
@@ -239,7 +239,11 @@ __global__ __launch_bounds__(64) void decode_f32_kernel(DecodeArgs p) {
       const int kk = i / CPR, c = i % CPR;
       const int j = t * kF32Keys + kk;
       f32x4 kv = {0.f, 0.f, 0.f, 0.f}, vv = kv;
-      if (j < n_sel) {
+      if (j < n_sel && p.compact) {
+        const size_t off = ((((size_t)b * p.Hkv + g) * n_sel) + j) * D + 4 * c;
+        kv = ld4(k_cache + off);
+        vv = ld4(v_cache + off);
+      } else if (j < n_sel) {
         const int q = j / (1 + p.Bt), s = j - q * (1 + p.Bt);
         const int slot = s == 0 ? 0 : tslot[q * p.Bt + s - 1];
         const size_t off = (cache_bg + (size_t)cidx[q] * p.Hkv * C1 + slot) * D + 4 * c;

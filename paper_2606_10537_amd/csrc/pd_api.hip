@@ -33,6 +33,7 @@ pd_status ok() {
 constexpr int kMaxChunks = 1024;
 constexpr int kMaxChunkLen = 4096;
 constexpr int kMaxSplits = 64;
+constexpr int kMaxCompactRows = 1 << 20;   // prefix rows of a compact decode call
 constexpr int kTargetWorkgroups = 256 * 8 / pd::kBf16Waves;  // two resident waves per SIMD on 256 CUs
 constexpr size_t kAlign = 256;
 
@@ -96,9 +97,11 @@ PrefillWs prefill_ws(const pd_dims* d) {
   return w;
 }
 
-// Chunk-score terms [B][N][H_q * row splits].
+// Chunk-score terms [B][N][H_q * row splits]; sized for the larger of the two
+// row sets a selection averages (L_d decode rows, or L_m pseudo-label rows).
 size_t select_ws(const pd_dims* d) {
-  return round_up((size_t)d->batch * d->n_chunks * d->n_heads_q * pd::select_row_splits(d->dec_len) * sizeof(float));
+  const int rows = std::max(d->dec_len, std::max(d->m_len, 1));
+  return round_up((size_t)d->batch * d->n_chunks * d->n_heads_q * pd::select_row_splits(rows) * sizeof(float));
 }
 
 int decode_qtiles(const pd_dims* d) {
@@ -110,33 +113,36 @@ int decode_units(const pd_dims* d) {
                              : d->batch * d->n_heads_q * decode_qtiles(d);
 }
 
-// Requested shard count: explicit, or chosen so that the decode grid reaches
-// about two workgroups per CU while every shard keeps >= 4 KV tiles of 64 rows.
-// The bf16 kernel also needs every shard to fit its LDS row table (at most
-// kDecodeTableRows rows, i.e. kDecodeTableRows/64 tiles), whatever n_static is.
-int min_splits(const pd_dims* d, int top_k, int tok_budget) {
-  const long long n_sel = (long long)top_k * (1 + tok_budget);
+// Shard counts for a decode call whose KV has n_sel prefix rows per (sequence,
+// KV head) ahead of the static and own rows.  Requested count: explicit, or
+// chosen so that the decode grid fills the CUs while every shard keeps >= 4 KV
+// tiles of 64 rows.  The bf16 kernel also needs every shard to fit its LDS row
+// table (at most kDecodeTableRows rows, i.e. kDecodeTableRows/64 tiles),
+// whatever n_static is.
+int min_splits(const pd_dims* d, long long n_sel) {
   if (d->dtype != PD_BF16 || n_sel <= pd::kDecodeTableRows) return 1;
   const long long lkv_max = n_sel + d->q_len + d->m_len + d->dec_len;
   return cdiv(cdiv(lkv_max, 64), pd::kDecodeTableRows / 64);
 }
 
-int requested_splits(const pd_dims* d, int top_k, int tok_budget, int num_splits) {
+int requested_splits(const pd_dims* d, long long n_sel, int num_splits) {
   int s = num_splits;
   if (s <= 0) {
-    const long long lkv0 = (long long)top_k * (1 + tok_budget) + d->dec_len;
+    const long long lkv0 = n_sel + d->dec_len;
     const int max_by_len = std::max(1, cdiv(lkv0, 64) / 4);
     const int want = cdiv(kTargetWorkgroups, std::max(1, decode_units(d)));
     s = std::max(1, std::min(std::min(want, max_by_len), kMaxSplits));
   }
-  return std::max(s, min_splits(d, top_k, tok_budget));
+  return std::max(s, min_splits(d, n_sel));
 }
 
-int effective_splits(const pd_dims* d, int top_k, int tok_budget, int n_static, int num_splits) {
-  const long long lkv = (long long)top_k * (1 + tok_budget) + n_static + d->dec_len;
+int effective_splits(const pd_dims* d, long long n_sel, int n_static, int num_splits) {
+  const long long lkv = n_sel + n_static + d->dec_len;
   const int tile = d->dtype == PD_BF16 ? 64 : 32;
-  return std::max(1, std::min(requested_splits(d, top_k, tok_budget, num_splits), cdiv(lkv, tile)));
+  return std::max(1, std::min(requested_splits(d, n_sel, num_splits), cdiv(lkv, tile)));
 }
+
+long long n_sel_of(int top_k, int tok_budget) { return (long long)top_k * (1 + tok_budget); }
 
 size_t decode_ws_bytes(const pd_dims* d, int S) {
   if (S <= 1) return 0;
@@ -210,14 +216,14 @@ size_t pd_workspace_bytes(const pd_dims* d, int32_t top_k, int32_t tok_budget, i
     case 1: return select_ws(d);
     case 2:
       if (top_k < 1 || tok_budget < 1 || num_splits < 0 || num_splits > kMaxSplits) return 0;
-      return decode_ws_bytes(d, requested_splits(d, top_k, tok_budget, num_splits));
+      return decode_ws_bytes(d, requested_splits(d, n_sel_of(top_k, tok_budget), num_splits));
     default: return 0;
   }
 }
 
 int32_t pd_decode_splits(const pd_dims* d, int32_t top_k, int32_t tok_budget, int32_t n_static, int32_t num_splits) {
   if (check_dims(d) != PD_OK || top_k < 1 || tok_budget < 1 || num_splits < 0 || num_splits > kMaxSplits) return 0;
-  return effective_splits(d, top_k, tok_budget, n_static, num_splits);
+  return effective_splits(d, n_sel_of(top_k, tok_budget), n_static, num_splits);
 }
 
 pd_status pd_prefill_chunks(const pd_dims* d, const void* q_pre, const void* k_pre, const void* v_pre,
@@ -344,22 +350,92 @@ pd_status pd_score_select(const pd_dims* d, int32_t top_k, int32_t tok_budget, c
   a.D = d->head_dim;
   a.K = top_k;
   a.Bt = tok_budget;
-  a.NS = pd::select_row_splits(d->dec_len);
+  a.q_rows = d->dec_len;
+  a.q_row0 = 0;
+  a.q_bstride = d->dec_len;
+  a.NS = pd::select_row_splits(a.q_rows);
   a.bf16 = d->dtype == PD_BF16;
   a.scale = scale_of(d);
   return hip_status(pd::launch_score_select(a, (hipStream_t)stream), "score/select kernels");
 }
 
-pd_status pd_sparse_decode_attn(const pd_dims* d, int32_t top_k, int32_t tok_budget, const void* q_dec,
-                                const void* k_dec, const void* v_dec, const void* k_cache, const void* v_cache,
-                                const int32_t* chunk_idx, const int32_t* tok_slot, const void* k_static,
-                                const void* v_static, int32_t n_static, void* o_dec, float* lse_dec,
-                                int32_t num_splits, void* workspace, size_t ws_bytes, void* stream) {
+pd_status pd_score_select_static(const pd_dims* d, int32_t top_k, int32_t tok_budget, const void* q_qm,
+                                 const float* key_mean, const int32_t* tok_rank, int32_t* chunk_idx,
+                                 int32_t* tok_slot, float* chunk_score, void* workspace, size_t ws_bytes,
+                                 void* stream) {
+  PD_RETURN_IF(check_dims(d));
+  if (d->m_len < 1) return fail(PD_ERR_BAD_DIMS, "m_len=%d: static selection needs pseudo-label rows", d->m_len);
+  if (top_k < 1 || top_k > d->n_chunks)
+    return fail(PD_ERR_BAD_DIMS, "top_k=%d must be in 1..n_chunks=%d", top_k, d->n_chunks);
+  if (tok_budget < 1 || tok_budget > d->chunk_len)
+    return fail(PD_ERR_BAD_DIMS, "tok_budget=%d must be in 1..chunk_len=%d", tok_budget, d->chunk_len);
+  PD_REQUIRE_PTR(q_qm);
+  PD_REQUIRE_PTR(key_mean);
+  PD_REQUIRE_PTR(tok_rank);
+  PD_REQUIRE_PTR(chunk_idx);
+  PD_REQUIRE_PTR(tok_slot);
+  if (chunk_score && !aligned16(chunk_score))
+    return fail(PD_ERR_MISALIGNED, "pointer 'chunk_score' is not 16-byte aligned");
+  PD_RETURN_IF(check_ws(workspace, ws_bytes, select_ws(d)));
+  pd::SelectArgs a{};
+  a.q_dec = q_qm;
+  a.key_mean = key_mean;
+  a.tok_rank = tok_rank;
+  a.partial = (float*)workspace;
+  a.chunk_score = chunk_score;
+  a.chunk_idx = chunk_idx;
+  a.tok_slot = tok_slot;
+  a.B = d->batch;
+  a.N = d->n_chunks;
+  a.C = d->chunk_len;
+  a.Hq = d->n_heads_q;
+  a.Hkv = d->n_heads_kv;
+  a.G = a.Hq / a.Hkv;
+  a.Ld = d->dec_len;
+  a.D = d->head_dim;
+  a.K = top_k;
+  a.Bt = tok_budget;
+  // The L_m pseudo-label rows follow the L_q query rows of each sequence's q/m
+  // block (chunk 0's copy when the rows are given per chunk).
+  a.q_rows = d->m_len;
+  a.q_row0 = d->q_len;
+  a.q_bstride = (d->qm_per_chunk ? d->n_chunks : 1) * (d->q_len + d->m_len);
+  a.NS = pd::select_row_splits(a.q_rows);
+  a.bf16 = d->dtype == PD_BF16;
+  a.scale = scale_of(d);
+  return hip_status(pd::launch_score_select(a, (hipStream_t)stream), "static score/select kernels");
+}
+
+pd_status pd_gather_selected(const pd_dims* d, int32_t top_k, int32_t tok_budget, const void* k_cache,
+                             const void* v_cache, const int32_t* chunk_idx, const int32_t* tok_slot, void* k_sel,
+                             void* v_sel, void* stream) {
   PD_RETURN_IF(check_dims(d));
   if (top_k < 1 || top_k > d->n_chunks)
     return fail(PD_ERR_BAD_DIMS, "top_k=%d must be in 1..n_chunks=%d", top_k, d->n_chunks);
   if (tok_budget < 1 || tok_budget > d->chunk_len)
     return fail(PD_ERR_BAD_DIMS, "tok_budget=%d must be in 1..chunk_len=%d", tok_budget, d->chunk_len);
+  PD_REQUIRE_PTR(k_cache);
+  PD_REQUIRE_PTR(v_cache);
+  PD_REQUIRE_PTR(chunk_idx);
+  PD_REQUIRE_PTR(tok_slot);
+  PD_REQUIRE_PTR(k_sel);
+  PD_REQUIRE_PTR(v_sel);
+  if ((long long)d->batch * d->n_heads_kv * n_sel_of(top_k, tok_budget) * d->head_dim * elem_bytes(d) / 16 >=
+      (1LL << 40))
+    return fail(PD_ERR_BAD_DIMS, "compact buffer too large");
+  return hip_status(pd::launch_gather_selected(k_cache, v_cache, chunk_idx, tok_slot, k_sel, v_sel, d->batch,
+                                               d->n_chunks, d->chunk_len, d->n_heads_kv, top_k, tok_budget,
+                                               d->head_dim * elem_bytes(d), (hipStream_t)stream),
+                    "gather kernel");
+}
+
+// Shared by the gathered and the compact decode entry points (arguments checked
+// by the caller except the common ones below).
+static pd_status decode_core(const pd_dims* d, int top_k, int tok_budget, long long n_sel, bool compact,
+                             const void* q_dec, const void* k_dec, const void* v_dec, const void* k_pref,
+                             const void* v_pref, const int32_t* chunk_idx, const int32_t* tok_slot,
+                             const void* k_static, const void* v_static, int32_t n_static, void* o_dec,
+                             float* lse_dec, int32_t num_splits, void* workspace, size_t ws_bytes, void* stream) {
   if (n_static < 0 || n_static > d->q_len + d->m_len)
     return fail(PD_ERR_BAD_DIMS, "n_static=%d must be in 0..q_len+m_len=%d", n_static, d->q_len + d->m_len);
   if (num_splits < 0 || num_splits > kMaxSplits)
@@ -367,18 +443,14 @@ pd_status pd_sparse_decode_attn(const pd_dims* d, int32_t top_k, int32_t tok_bud
   PD_REQUIRE_PTR(q_dec);
   PD_REQUIRE_PTR(k_dec);
   PD_REQUIRE_PTR(v_dec);
-  PD_REQUIRE_PTR(k_cache);
-  PD_REQUIRE_PTR(v_cache);
-  PD_REQUIRE_PTR(chunk_idx);
-  PD_REQUIRE_PTR(tok_slot);
   PD_REQUIRE_PTR(o_dec);
   if (n_static > 0) {
     PD_REQUIRE_PTR(k_static);
     PD_REQUIRE_PTR(v_static);
   }
   if (lse_dec && !aligned16(lse_dec)) return fail(PD_ERR_MISALIGNED, "pointer 'lse_dec' is not 16-byte aligned");
-  const int S_req = requested_splits(d, top_k, tok_budget, num_splits);
-  const int S = effective_splits(d, top_k, tok_budget, n_static, num_splits);
+  const int S_req = requested_splits(d, n_sel, num_splits);
+  const int S = effective_splits(d, n_sel, n_static, num_splits);
   PD_RETURN_IF(check_ws(workspace, ws_bytes, decode_ws_bytes(d, S_req)));
 
   const bool bf16 = d->dtype == PD_BF16;
@@ -387,8 +459,8 @@ pd_status pd_sparse_decode_attn(const pd_dims* d, int32_t top_k, int32_t tok_bud
   a.q_dec = (const uint16_t*)q_dec;
   a.k_dec = (const uint16_t*)k_dec;
   a.v_dec = (const uint16_t*)v_dec;
-  a.k_cache = (const uint16_t*)k_cache;
-  a.v_cache = (const uint16_t*)v_cache;
+  a.k_cache = (const uint16_t*)k_pref;
+  a.v_cache = (const uint16_t*)v_pref;
   a.k_static = (const uint16_t*)k_static;
   a.v_static = (const uint16_t*)v_static;
   a.chunk_idx = chunk_idx;
@@ -405,6 +477,8 @@ pd_status pd_sparse_decode_attn(const pd_dims* d, int32_t top_k, int32_t tok_bud
   a.Ls = d->q_len + d->m_len;
   a.K = top_k;
   a.Bt = tok_budget;
+  a.n_sel = (int)n_sel;
+  a.compact = compact ? 1 : 0;
   a.n_static = n_static;
   a.S = S;
   a.out_f32 = d->out_fp32;
@@ -423,7 +497,48 @@ pd_status pd_sparse_decode_attn(const pd_dims* d, int32_t top_k, int32_t tok_bud
                            bf16 && !d->out_fp32, s);
     if (err != hipSuccess) return hip_status(err, "merge kernel");
   }
-  return ok();
+  return PD_OK;
+}
+
+pd_status pd_sparse_decode_attn(const pd_dims* d, int32_t top_k, int32_t tok_budget, const void* q_dec,
+                                const void* k_dec, const void* v_dec, const void* k_cache, const void* v_cache,
+                                const int32_t* chunk_idx, const int32_t* tok_slot, const void* k_static,
+                                const void* v_static, int32_t n_static, void* o_dec, float* lse_dec,
+                                int32_t num_splits, void* workspace, size_t ws_bytes, void* stream) {
+  PD_RETURN_IF(check_dims(d));
+  if (top_k < 1 || top_k > d->n_chunks)
+    return fail(PD_ERR_BAD_DIMS, "top_k=%d must be in 1..n_chunks=%d", top_k, d->n_chunks);
+  if (tok_budget < 1 || tok_budget > d->chunk_len)
+    return fail(PD_ERR_BAD_DIMS, "tok_budget=%d must be in 1..chunk_len=%d", tok_budget, d->chunk_len);
+  PD_REQUIRE_PTR(k_cache);
+  PD_REQUIRE_PTR(v_cache);
+  PD_REQUIRE_PTR(chunk_idx);
+  PD_REQUIRE_PTR(tok_slot);
+  return decode_core(d, top_k, tok_budget, n_sel_of(top_k, tok_budget), false, q_dec, k_dec, v_dec, k_cache,
+                     v_cache, chunk_idx, tok_slot, k_static, v_static, n_static, o_dec, lse_dec, num_splits,
+                     workspace, ws_bytes, stream);
+}
+
+pd_status pd_sparse_decode_attn_compact(const pd_dims* d, int32_t n_sel, const void* q_dec, const void* k_dec,
+                                        const void* v_dec, const void* k_sel, const void* v_sel,
+                                        const void* k_static, const void* v_static, int32_t n_static, void* o_dec,
+                                        float* lse_dec, int32_t num_splits, void* workspace, size_t ws_bytes,
+                                        void* stream) {
+  PD_RETURN_IF(check_dims(d));
+  if (n_sel < 0 || n_sel > kMaxCompactRows)
+    return fail(PD_ERR_BAD_DIMS, "n_sel=%d must be in 0..%d", n_sel, kMaxCompactRows);
+  if (n_sel > 0) {
+    PD_REQUIRE_PTR(k_sel);
+    PD_REQUIRE_PTR(v_sel);
+  }
+  return decode_core(d, 0, 0, n_sel, true, q_dec, k_dec, v_dec, k_sel, v_sel, nullptr, nullptr, k_static,
+                     v_static, n_static, o_dec, lse_dec, num_splits, workspace, ws_bytes, stream);
+}
+
+size_t pd_compact_workspace_bytes(const pd_dims* d, int32_t n_sel, int32_t num_splits) {
+  if (check_dims(d) != PD_OK || n_sel < 0 || n_sel > kMaxCompactRows || num_splits < 0 || num_splits > kMaxSplits)
+    return 0;
+  return decode_ws_bytes(d, requested_splits(d, n_sel, num_splits));
 }
 
 }  // extern "C"

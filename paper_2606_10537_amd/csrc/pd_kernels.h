@@ -59,6 +59,8 @@ struct DecodeArgs {
   float* o_part;     // [S][B][Hq][Ld][D] shard outputs (normalised), S > 1
   float* lse_part;   // [S][B][Hq][Ld] log2-domain shard LSE, S > 1
   int B, N, C, Hq, Hkv, G, Ld, Ls, K, Bt, n_static, S;
+  int n_sel;         // prefix rows per (sequence, KV head): K*(1+Bt) gathered, or the compact count
+  int compact;       // 1: prefix rows j < n_sel are rows of k_cache/v_cache laid out [B][Hkv][n_sel][D]
   int n_qt, total;
   int out_f32;       // o_dec is fp32 instead of the input element type
   float scale_log2;
@@ -90,10 +92,14 @@ struct SelectArgs {
   float* chunk_score;  // [B][N] or nullptr
   int32_t *chunk_idx, *tok_slot;
   int B, N, C, Hq, Hkv, G, Ld, D, K, Bt, NS;
+  int q_rows, q_row0, q_bstride;   // rows averaged into the mean query: rows q_row0.. of q_bstride per sequence
   bool bf16;
   float scale;
 };
 hipError_t launch_score_select(const SelectArgs& a, hipStream_t s);
+hipError_t launch_gather_selected(const void* k_cache, const void* v_cache, const int32_t* chunk_idx,
+                                  const int32_t* tok_slot, void* k_sel, void* v_sel, int B, int N, int C, int Hkv,
+                                  int K, int Bt, int row_bytes, hipStream_t s);
 hipError_t launch_mfma_rate(int n_workgroups, int iters, float* sink, hipStream_t s);
 hipError_t launch_token_rank(const float* tok_score, int32_t* tok_rank, int B, int N, int C, hipStream_t s);
 int select_row_splits(int Ld);

@@ -8,6 +8,8 @@
 //                                  over heads and row splits: one workgroup sums
 //                                  its rows of one head, then dots with all N
 //                                  key means of that head's KV group;
+//   gather:     grid (rows)     -- static-selection mode: kept rows copied once
+//                                  into a contiguous per-(sequence, KV head) buffer;
 //   select:     grid (b, k)     -- sums the terms of every chunk in a fixed
 //                                  order, ranks the N scores (bitonic sort in
 //                                  LDS), takes the k-th kept chunk in ascending
@@ -131,15 +133,17 @@ int select_row_splits(int Ld) { return (Ld + kScoreRows - 1) / kScoreRows; }
 // flight at once), reduced by a fixed xor butterfly.
 template <bool BF16, int D>
 __global__ __launch_bounds__(256) void qscore_kernel(const void* q_dec, const float* key_mean, float* partial,
-                                                      int N, int Hq, int Hkv, int G, int Ld, int NS, float scale) {
+                                                      int N, int Hq, int Hkv, int G, int rows, int row0, int bstride,
+                                                      int NS, float scale) {
   constexpr int SL = D / 8;
   __shared__ float red[2048];
   __shared__ float qp[D];
   const int sp = blockIdx.x % NS;
   const int bh = blockIdx.x / NS;
   const int h = bh % Hq, b = bh / Hq;
-  const int r0 = sp * kScoreRows, r1 = min(Ld, r0 + kScoreRows);
-  rows_mean<BF16>(q_dec, (((size_t)b * Ld + r0) * Hq + h) * D, (size_t)Hq * D, r1 - r0, D, 1.0f / Ld, qp, red);
+  const int r0 = sp * kScoreRows, r1 = min(rows, r0 + kScoreRows);
+  rows_mean<BF16>(q_dec, (((size_t)b * bstride + row0 + r0) * Hq + h) * D, (size_t)Hq * D, r1 - r0, D, 1.0f / rows,
+                  qp, red);
   __syncthreads();
   const float* kb = key_mean + ((size_t)b * N * Hkv + h / G) * D;
   const int j = threadIdx.x & 7;
@@ -236,7 +240,7 @@ hipError_t launch_score_select(const SelectArgs& a, hipStream_t s) {
   const dim3 g1(a.B * a.Hq * a.NS);
 #define PD_QSCORE(BF, DD)                                                                                      \
   hipLaunchKernelGGL((qscore_kernel<BF, DD>), g1, dim3(256), 0, s, a.q_dec, a.key_mean, a.partial, a.N, a.Hq, \
-                     a.Hkv, a.G, a.Ld, a.NS, a.scale)
+                     a.Hkv, a.G, a.q_rows, a.q_row0, a.q_bstride, a.NS, a.scale)
   if (a.D == 128) {
     if (a.bf16) PD_QSCORE(true, 128); else PD_QSCORE(false, 128);
   } else {
@@ -248,6 +252,40 @@ hipError_t launch_score_select(const SelectArgs& a, hipStream_t s) {
   const int Npad = next_pow2(a.N);
   hipLaunchKernelGGL(select_kernel, dim3(a.B * a.K), dim3(256), (size_t)Npad * 8, s, a.partial, a.tok_rank,
                      a.chunk_score, a.chunk_idx, a.tok_slot, a.N, a.C, a.K, a.Bt, a.Hq * a.NS, Npad);
+  return hipGetLastError();
+}
+
+// Static-selection mode: copy the kept rows of every (sequence, KV head) into a
+// contiguous buffer [B][Hkv][K*(1+Bt)][row]: per kept chunk (ascending), its BOS
+// row (slot 0) and then its kept slots.  16 bytes per thread.
+__global__ __launch_bounds__(256) void gather_selected_kernel(const u32x4* k_cache, const u32x4* v_cache,
+                                                               const int32_t* chunk_idx, const int32_t* tok_slot,
+                                                               u32x4* k_sel, u32x4* v_sel, size_t total, int N,
+                                                               int C1, int Hkv, int K, int Bt, int cpr) {
+  const size_t gid = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (gid >= total) return;
+  const int n_sel = K * (1 + Bt);
+  const int c = (int)(gid % cpr);
+  size_t r = gid / cpr;
+  const int j = (int)(r % n_sel);
+  r /= n_sel;
+  const int g = (int)(r % Hkv);
+  const int b = (int)(r / Hkv);
+  const int kk = j / (1 + Bt), sl = j - kk * (1 + Bt);
+  const int slot = sl == 0 ? 0 : tok_slot[((size_t)b * K + kk) * Bt + sl - 1];
+  const size_t src = ((((size_t)b * N + chunk_idx[(size_t)b * K + kk]) * Hkv + g) * C1 + slot) * cpr + c;
+  k_sel[gid] = k_cache[src];
+  v_sel[gid] = v_cache[src];
+}
+
+hipError_t launch_gather_selected(const void* k_cache, const void* v_cache, const int32_t* chunk_idx,
+                                  const int32_t* tok_slot, void* k_sel, void* v_sel, int B, int N, int C, int Hkv,
+                                  int K, int Bt, int row_bytes, hipStream_t s) {
+  const int cpr = row_bytes / 16;
+  const size_t total = (size_t)B * Hkv * K * (1 + Bt) * cpr;
+  const dim3 grid((unsigned)((total + 255) / 256));
+  hipLaunchKernelGGL(gather_selected_kernel, grid, dim3(256), 0, s, (const u32x4*)k_cache, (const u32x4*)v_cache,
+                     chunk_idx, tok_slot, (u32x4*)k_sel, (u32x4*)v_sel, total, N, C + 1, Hkv, K, Bt, cpr);
   return hipGetLastError();
 }
 

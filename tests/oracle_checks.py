@@ -28,6 +28,7 @@ import torch
 import oracle.decode as OD
 import oracle.prefill as OP
 import oracle.select as OS
+import oracle.static as OT
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 
@@ -351,3 +352,74 @@ def check_decode_permutation(seed):
     o2, l2 = _decode(x, ci[:, ::-1].copy(), ts[:, ::-1, ::-1].copy(), 2)
     np.testing.assert_allclose(o1, o2, atol=1e-12)
     np.testing.assert_allclose(l1, l2, atol=1e-12)
+
+
+# --- static-selection mode ---------------------------------------------------------------------------------------
+
+def check_static_golden():
+    g = _load("static_worked_example.json")
+    q_qm = np.array(g["q_qm"], float)
+    km = np.array(g["key_mean"], float)
+    ts = np.array(g["tok_score"], float)
+    dm = g["dims"]
+    ci, sl, sc = OT.static_select_ref(q_qm, km, ts, dm["top_k"], dm["tok_budget"], dm["q_len"], dm["scale"])
+    np.testing.assert_allclose(sc, np.array(g["expect_scores"], float), atol=1e-12)
+    assert np.array_equal(ci, np.array(g["expect_chunk_idx"]))
+    assert np.array_equal(sl, np.array(g["expect_tok_slot"]))
+    cache = np.zeros((1, 2, 1, 4, 2))
+    for n in range(2):
+        for slot in range(4):
+            cache[0, n, 0, slot] = [10 * n + slot, -(10 * n + slot)]
+    np.testing.assert_array_equal(OT.gather_selected_ref(cache, ci, sl), np.array(g["expect_k_sel"], float))
+
+
+def _tiny_selection(seed, B, N, C, K, Bt):
+    rng = np.random.default_rng(seed + 100)
+    ci = np.stack([np.sort(rng.permutation(N)[:K]) for _ in range(B)]).astype(np.int32)
+    ts = np.stack([np.stack([np.sort(rng.permutation(C)[:Bt] + 1) for _ in range(K)]) for _ in range(B)])
+    return ci, ts.astype(np.int32)
+
+
+def check_gather_matches_decode_rows(seed):
+    """The compact rows of (b, g) are the first K(1+B_tok) rows the per-step decode reads."""
+    B, N, C, Hkv, d, K, Bt = 2, 4, 6, 2, 8, 2, 3
+    x = tiny_decode_inputs(seed, B, N, C, 3, 4, 4, Hkv, d)
+    ci, ts = _tiny_selection(seed, B, N, C, K, Bt)
+    ks = OT.gather_selected_ref(x["k_cache"], ci, ts)
+    for b in range(B):
+        for g in range(Hkv):
+            rows = OD.decode_kv_rows(x["k_cache"], x["k_static"], x["k_dec"], ci, ts, 0, b, g)
+            np.testing.assert_array_equal(ks[b, g], rows[:K * (1 + Bt)])
+
+
+def check_compact_decode_equals_gathered(seed, n_static):
+    """Decode over the compacted rows equals the per-step decode with the same selection."""
+    B, N, C, Hkv, d, K, Bt = 2, 4, 6, 2, 8, 3, 4
+    x = tiny_decode_inputs(seed, B, N, C, 3, 4, 4, Hkv, d)
+    ci, ts = _tiny_selection(seed, B, N, C, K, Bt)
+    ks, vs = OT.gather_selected_ref(x["k_cache"], ci, ts), OT.gather_selected_ref(x["v_cache"], ci, ts)
+    o1, l1 = OT.decode_compact_ref(x["q_dec"], x["k_dec"], x["v_dec"], ks, vs, x["k_static"], x["v_static"], n_static)
+    o2, l2 = _decode(x, ci, ts, n_static)
+    np.testing.assert_allclose(o1, o2, atol=1e-12)
+    np.testing.assert_allclose(l1, l2, atol=1e-12)
+
+
+def check_compact_decode_sdpa(seed):
+    """An arbitrary compact buffer: dense attention over [compact ; static ; own] (torch SDPA, float64)."""
+    B, Ld, Ls, Hq, Hkv, d, n_sel, n_static = 2, 3, 4, 4, 2, 8, 5, 3
+    rng = np.random.default_rng(seed)
+    x = tiny_decode_inputs(seed, B, 2, 2, Ld, Ls, Hq, Hkv, d)
+    ks, vs = rng.standard_normal((B, Hkv, n_sel, d)), rng.standard_normal((B, Hkv, n_sel, d))
+    o, lse = OT.decode_compact_ref(x["q_dec"], x["k_dec"], x["v_dec"], ks, vs, x["k_static"], x["v_static"], n_static)
+    scale = 1.0 / np.sqrt(d)
+    for b in range(B):
+        for h in range(Hq):
+            g = h // (Hq // Hkv)
+            k = np.concatenate([ks[b, g], x["k_static"][b, :n_static, g], x["k_dec"][b, :, g]])
+            v = np.concatenate([vs[b, g], x["v_static"][b, :n_static, g], x["v_dec"][b, :, g]])
+            q = torch.from_numpy(x["q_dec"][b, :, h])
+            ot = torch.nn.functional.scaled_dot_product_attention(q[None], torch.from_numpy(k)[None],
+                                                                  torch.from_numpy(v)[None])[0]
+            np.testing.assert_allclose(o[b, :, h], ot.numpy(), atol=1e-12)
+            lt = torch.logsumexp(scale * q @ torch.from_numpy(k).T, dim=1).numpy()
+            np.testing.assert_allclose(lse[b, h], lt, atol=1e-12)

@@ -119,6 +119,33 @@ def test_decode_validation(lib):
     assert call(splits=4, w=None) == 5
 
 
+def test_static_mode_validation(lib):
+    d = dims()
+    c = ctypes.byref(d.c())
+    ws = _lib.pd_workspace_bytes(d, 2, 64, 0, 1)
+    sel = lambda k=2, bt=64, q=A, wn=ws, dd=c: lib.pd_score_select_static(dd, k, bt, q, A, A, A, A, None, A, wn, None)
+    assert sel(k=0) == 2
+    assert sel(bt=129) == 2
+    assert sel(q=None) == 1
+    assert sel(wn=ws - 1) == 5
+    assert sel(dd=ctypes.byref(dims(m_len=0).c())) == 2
+    gat = lambda k=2, bt=64, ks=A: lib.pd_gather_selected(c, k, bt, A, A, A, A, ks, A, None)
+    assert gat(k=5) == 2
+    assert gat(bt=0) == 2
+    assert gat(ks=None) == 1
+    cmp_ = lambda n=10, ks=A, ns=16, sp=0, lse=None: lib.pd_sparse_decode_attn_compact(
+        c, n, A, A, A, ks, ks, A, A, ns, A, lse, sp, A, 1 << 30, None)
+    assert cmp_(n=-1) == 2
+    assert cmp_(n=(1 << 20) + 1) == 2
+    assert cmp_(ks=None) == 1
+    assert cmp_(ns=49) == 2
+    assert cmp_(sp=65) == 2
+    assert cmp_(lse=MIS) == 4
+    assert _lib.pd_compact_workspace_bytes(d, -1, 0) == 0
+    assert _lib.pd_compact_workspace_bytes(d, 100, 1) == 0
+    assert _lib.pd_compact_workspace_bytes(d, 100, 3) >= 3 * 1 * 4 * 32 * 65 * 4
+
+
 def test_mfma_probe_validation(lib):
     assert lib.pd_mfma_rate_probe(0, 10, A, None) == 2
     assert lib.pd_mfma_rate_probe(4, 0, A, None) == 2

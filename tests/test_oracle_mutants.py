@@ -10,6 +10,7 @@ import pytest
 import oracle.decode as OD
 import oracle.prefill as OP
 import oracle.select as OS
+import oracle.static as OT
 import oracle_checks as C
 
 
@@ -107,6 +108,16 @@ def _rows_slot_off_by_one(x_cache, x_static, x_dec, chunk_idx, tok_slot, n_stati
     return _orig_rows(x_cache, x_static, x_dec, chunk_idx, np.asarray(tok_slot) - 1, n_static, b, g)
 
 
+def _gather_no_bos(x_cache, chunk_idx, tok_slot):
+    x = np.asarray(x_cache)
+    ci, ts = np.asarray(chunk_idx), np.asarray(tok_slot)
+    out = []
+    for b in range(x.shape[0]):
+        out.append(np.stack([np.concatenate([x[b, int(n), g, ts[b, kk]] for kk, n in enumerate(ci[b])])
+                             for g in range(x.shape[2])]))
+    return np.stack(out)
+
+
 MUTANTS = [
     ("softmax over columns", OP, "chunk_probs", _softmax_cols,
      [C.check_prefill_golden, lambda: C.check_prefill_sdpa(3)]),
@@ -132,6 +143,13 @@ MUTANTS = [
      [C.check_decode_golden, lambda: C.check_decode_dense(14)]),
     ("decode slot off by one", OD, "decode_kv_rows", _rows_slot_off_by_one,
      [C.check_decode_golden]),
+    ("static selection averages every q/m row", OT, "pseudo_label_queries", lambda q_qm, q_len: np.asarray(q_qm),
+     [C.check_static_golden]),
+    ("static selection uses the query rows", OT, "pseudo_label_queries",
+     lambda q_qm, q_len: np.asarray(q_qm)[:, :q_len], [C.check_static_golden]),
+    ("gather drops the chunk BOS rows", OT, "gather_selected_ref", _gather_no_bos,
+     [C.check_static_golden, lambda: C.check_gather_matches_decode_rows(1),
+      lambda: C.check_compact_decode_equals_gathered(7, 3)]),
 ]
 
 

@@ -75,3 +75,21 @@ def test_decode_dense(n_static):
 
 def test_decode_permutation():
     C.check_decode_permutation(15)
+
+
+def test_static_golden():
+    C.check_static_golden()
+
+
+@pytest.mark.parametrize("seed", [1, 2])
+def test_gather_matches_decode_rows(seed):
+    C.check_gather_matches_decode_rows(seed)
+
+
+@pytest.mark.parametrize("n_static", [0, 3])
+def test_compact_decode_equals_gathered(n_static):
+    C.check_compact_decode_equals_gathered(7, n_static)
+
+
+def test_compact_decode_sdpa():
+    C.check_compact_decode_sdpa(5)
