@@ -38,6 +38,8 @@ def parse():
     p.add_argument("--flush-mib", type=int, default=0,
                    help="write this many MiB before every decode launch, so that each launch starts with the "
                         "last-level cache (MALL) holding none of its operands (cold numbers)")
+    p.add_argument("--no-static", action="store_true",
+                   help="skip the static-selection-mode measurement after the timed region")
     p.add_argument("--no-achievable", action="store_true",
                    help="skip the achievable-peak measurements (library GEMM, device copy) after the timed region")
     p.add_argument("--calib-copy-mib", type=int, default=0,
@@ -138,6 +140,69 @@ def cpu_baseline(w, budget_s):
                    f"({B * N * Hq * L} prefill, {B * T * L} select, {B * Hq * T * L} decode units); extrapolated"),
         "seconds_per_step_extrapolated": step_s,
     }
+
+
+def static_mode(torch, _lib, w, d, pool, dec_pool, k_cache, v_cache, key_mean, tok_rank, stream, dec_flop,
+                pre_ms_layer, n_static):
+    """Static-selection mode on the same caches, measured after the timed region: per layer one
+    selection from the pseudo-label rows and one gather of the kept rows into a compact buffer, then
+    the T-step loop of compact decodes (HIP events around every decode launch)."""
+    dev = "cuda"
+    L, T, K, Bt = w.layers, w.steps, w.top_k, w.tok_budget
+    B, Hkv, D = w.batch, w.n_heads_kv, w.head_dim
+    n_sel = K * (1 + Bt)
+    sh = stream.cuda_stream
+    ws_sel = torch.empty(_lib.pd_workspace_bytes(d, K, Bt, 0, 1), dtype=torch.uint8, device=dev)
+    ws_dec = torch.empty(max(16, _lib.pd_compact_workspace_bytes(d, n_sel, 0)), dtype=torch.uint8, device=dev)
+    ci = torch.empty((B, K), dtype=torch.int32, device=dev)
+    ts = torch.empty((B, K, Bt), dtype=torch.int32, device=dev)
+    k_sel = [torch.empty((B, Hkv, n_sel, D), dtype=w.torch_dtype, device=dev) for _ in range(L)]
+    v_sel = [torch.empty_like(k_sel[0]) for _ in range(L)]
+    o_dec = torch.empty((B, w.dec_len, w.n_heads_q, D), dtype=w.torch_dtype, device=dev)
+    dec_slots = len(dec_pool[0])
+
+    def select_gather():
+        for l in range(L):
+            _lib.pd_score_select_static(d, K, Bt, pool[l % len(pool)]["q_qm"], key_mean[l], tok_rank[l], ci, ts,
+                                        None, ws_sel, sh)
+            _lib.pd_gather_selected(d, K, Bt, k_cache[l], v_cache[l], ci, ts, k_sel[l], v_sel[l], sh)
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(L * T)]
+
+    def loop(record):
+        i = 0
+        for t in range(T):
+            for l in range(L):
+                dd = dec_pool[l][t % dec_slots]
+                if record:
+                    ev[i][0].record(stream)
+                _lib.pd_sparse_decode_attn_compact(d, n_sel, dd["q_dec"], dd["k_dec"], dd["v_dec"], k_sel[l],
+                                                   v_sel[l], pool[l % len(pool)]["k_qm"],
+                                                   pool[l % len(pool)]["v_qm"], n_static, o_dec, None, 0, ws_dec, sh)
+                if record:
+                    ev[i][1].record(stream)
+                i += 1
+
+    select_gather()
+    loop(False)
+    torch.cuda.synchronize()
+    s0, s1, s2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    s0.record(stream)
+    select_gather()
+    s1.record(stream)
+    loop(True)
+    s2.record(stream)
+    torch.cuda.synchronize()
+    sg_ms = s0.elapsed_time(s1)
+    loop_ms = s1.elapsed_time(s2)
+    launch_ms = sum(a.elapsed_time(b) for a, b in ev) / len(ev)
+    return {"steps_per_s": round(T / (loop_ms * 1e-3), 3),
+            "job_steps_per_s": round(T / ((pre_ms_layer * L + sg_ms + loop_ms) * 1e-3), 3),
+            "select_gather_ms_per_layer": round(sg_ms / L, 4),
+            "decode_launch_ms": round(launch_ms, 5),
+            "decode_tflops": round(dec_flop / (launch_ms * 1e-3) / 1e12, 2),
+            "note": "selection once per layer from the pseudo-label rows, kept rows compacted once; decode over "
+                    "the compact buffer; same caches, decode inputs and flop count as the per-step mode"}
 
 
 def achievable_peaks(torch, dev):
@@ -321,6 +386,9 @@ def main():
         "roofline": roof,
         "wall_s": round(wall, 3),
     }
+    if not args.no_static:
+        res["static_mode"] = static_mode(torch, _lib, w, d, pool, dec_pool, k_cache, v_cache, key_mean, tok_rank,
+                                         stream, dec_flop, pre_ms_layer, n_static)
     if not args.no_achievable:
         ach = achievable_peaks(torch, dev)
         res["achievable"] = ach
