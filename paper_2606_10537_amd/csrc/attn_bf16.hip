@@ -73,9 +73,15 @@ __device__ __forceinline__ i16x4 ld_tr16(const uint16_t* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((PD_LDS i16x4*)(p));
 }
 
-// 16 bytes from global memory into LDS slot `lane` of the 1 KB block at lds.
+// 16 bytes from global memory into LDS slot `lane` of the 1 KB block at lds
+// (global_load_lds_dwordx4 with the block's LDS address in M0).  Issued as
+// inline assembly: when the compiler sees an LDS DMA in flight it can no longer
+// count LDS reads precisely and waits for all of them (lgkmcnt(0)) before every
+// fragment use.  Completion is tracked by hand (wait_dma_keep); loads the
+// compiler does not see only make its own vmcnt waits stricter.
 __device__ __forceinline__ void dma16(const uint16_t* g, uint16_t* lds) {
-  __builtin_amdgcn_global_load_lds(g, (PD_LDS void*)(lds), 16, 0, 0);
+  const uint32_t lds_addr = (uint32_t)(uintptr_t)(PD_LDS void*)(lds);
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_addr) : "memory", "m0");
 }
 
 // Engine state of 32 query rows of a wave (a wave holds NH of them).
@@ -120,31 +126,40 @@ __device__ __forceinline__ bf16x8 k_frag(const uint16_t* Ks, const FragAddr& fa,
   return __builtin_bit_cast(bf16x8, ld16(Ks + fa.k[ks & 1] + (ks >> 1) * 2048 + kb * 1024));
 }
 
-// Fragments are read two k-steps ahead of the MFMAs that use them; each K
-// fragment serves the NH row groups of the wave.
+// Fragments are read PF k-steps ahead of the MFMAs that use them (kept in that
+// order by scheduling fences); each K fragment serves the NH row groups.
+#ifndef PD_S_PREFETCH
+#define PD_S_PREFETCH 2
+#endif
+#ifndef PD_PIN_S
+#define PD_PIN_S 1
+#endif
 template <int D, int NH>
 __device__ __forceinline__ void s_phase(f32x16 (&s)[NH][2], const WaveState<D> (&st)[NH], const uint16_t* Ks,
                                         const FragAddr& fa) {
   using T = Tile<D>;
+  constexpr int PF = PD_S_PREFETCH < T::KS ? PD_S_PREFETCH : T::KS - 1;
 #pragma unroll
   for (int h = 0; h < NH; ++h)
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) s[h][kb] = f32x16{0};
-  bf16x8 a[3][2];
+  bf16x8 a[PF + 1][2];
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks)
+  for (int ks = 0; ks < PF; ++ks)
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) a[ks][kb] = k_frag<D>(Ks, fa, ks, kb);
 #pragma unroll
   for (int ks = 0; ks < T::KS; ++ks) {
-    if (ks + 2 < T::KS) {
+    if (ks + PF < T::KS) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) a[(ks + 2) % 3][kb] = k_frag<D>(Ks, fa, ks + 2, kb);
+      for (int kb = 0; kb < 2; ++kb) a[(ks + PF) % (PF + 1)][kb] = k_frag<D>(Ks, fa, ks + PF, kb);
     }
+    if (PD_PIN_S) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int h = 0; h < NH; ++h) s[h][kb] = mfma32x32x16(a[ks % 3][kb], st[h].qf[ks], s[h][kb]);
+      for (int h = 0; h < NH; ++h) s[h][kb] = mfma32x32x16(a[ks % (PF + 1)][kb], st[h].qf[ks], s[h][kb]);
+    if (PD_PIN_S) __builtin_amdgcn_sched_barrier(0);
   }
 }
 
