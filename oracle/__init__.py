@@ -20,6 +20,9 @@ that each step can be checked against the paper by eye:
   prefix KV, the static query KV and its own KV (Section 5.3, prefix reuse).
 * ``static``   -- static-selection mode: selection once from the pseudo-label
   rows, the kept rows compacted into a contiguous buffer, decode over it.
+* ``chunk_score`` -- the prefill-time chunk score built from the attention
+  mass the query and pseudo-label rows put on the chunk content (an
+  attention-space reading of Eqs. 3-4), and selection of the K lowest.
 
 Parity status of each function is stated in its docstring ("pinned by ...").
 """
@@ -41,6 +44,7 @@ from .static import (
     decode_compact_unit_ref,
     decode_compact_ref,
 )
+from .chunk_score import prefill_chunk_score_ref, select_ranked_ref
 
 __all__ = [
     "chunk_rows",
@@ -62,4 +66,6 @@ __all__ = [
     "gather_selected_ref",
     "decode_compact_unit_ref",
     "decode_compact_ref",
+    "prefill_chunk_score_ref",
+    "select_ranked_ref",
 ]

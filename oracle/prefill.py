@@ -17,6 +17,12 @@ sparsity", Eq. 5) of the paper.  Readings taken where the paper is silent:
   part in the normalisation.  BOS is not a candidate token.
 * The chunk key summary used by the per-step chunk score is the mean of the C
   content keys of the chunk (BOS excluded), per KV head.
+* The query-to-chunk variant of the token score (the paper's ablation of the
+  retention score) keeps only the first sum of Eq. 5: the mass the query rows
+  put on the token.
+* The content mass of a query or pseudo-label row is the probability it puts
+  on the C content columns of its chunk (BOS excluded); the prefill-time chunk
+  score (``oracle.chunk_score``) is built from it.
 
 Layouts (numpy, any float dtype on input, float64 inside):
   q_pre (B, N, 1+C, Hq, d), k_pre / v_pre (B, N, 1+C, Hkv, d), slot 0 = BOS;
@@ -64,7 +70,9 @@ def prefill_unit_ref(q_pre, k_pre, v_pre, q_qm, k_qm, v_qm, b, n, h, q_len, scal
       o      (S_c, d)  attention output rows, ordered BOS, c, q, m (Eq. 2 forward);
       p      (S_c, S_c) the probabilities;
       lse    (S_c,)    natural-log row LSE;
-      e_head (C,)      this head's contribution to Eq. 5 for the C content tokens.
+      e_head (C,)      this head's contribution to Eq. 5 for the C content tokens;
+      e_q2c_head (C,)  its first sum only (query rows -> content columns);
+      content_mass (Lq+Lm,) mass of each q/m row on the C content columns.
     """
     hq, hkv = q_pre.shape[3], k_pre.shape[3]
     d = q_pre.shape[4]
@@ -80,8 +88,11 @@ def prefill_unit_ref(q_pre, k_pre, v_pre, q_qm, k_qm, v_qm, b, n, h, q_len, scal
     content = slice(1, c1)            # slots 1..C
     qrows = slice(c1, c1 + q_len)     # the L_q query rows
     # Eq. 5: query row -> content column, plus content row -> query column.
-    e_head = p[qrows, content].sum(axis=0) + p[content, qrows].sum(axis=1)
-    return {"o": o, "p": p, "lse": lse, "e_head": e_head}
+    e_q2c_head = p[qrows, content].sum(axis=0)
+    e_head = e_q2c_head + p[content, qrows].sum(axis=1)
+    content_mass = p[c1:, content].sum(axis=1)
+    return {"o": o, "p": p, "lse": lse, "e_head": e_head, "e_q2c_head": e_q2c_head,
+            "content_mass": content_mass}
 
 
 def cache_ref(x_pre):
@@ -102,8 +113,9 @@ def prefill_ref(q_pre, k_pre, v_pre, q_qm, k_qm, v_qm, q_len, scale=None):
     """Whole stage (a) for small inputs.
 
     Returns dict: o (B, N, S_c, Hq, d), k_cache / v_cache (B, N, Hkv, 1+C, d,
-    input dtype), tok_score (B, N, C) = Eq. 5 summed over heads, key_mean
-    (B, N, Hkv, d), lse (B, N, Hq, S_c).
+    input dtype), tok_score (B, N, C) = Eq. 5 summed over heads,
+    tok_score_q2c (B, N, C) = its first sum only, key_mean (B, N, Hkv, d),
+    lse (B, N, Hq, S_c), content_mass (B, N, Hq, Lq+Lm).
     """
     bsz, nch, c1, hq, d = q_pre.shape
     lqm = q_qm.shape[-3]
@@ -111,6 +123,8 @@ def prefill_ref(q_pre, k_pre, v_pre, q_qm, k_qm, v_qm, q_len, scale=None):
     o = np.zeros((bsz, nch, sc, hq, d))
     lse = np.zeros((bsz, nch, hq, sc))
     tok = np.zeros((bsz, nch, c1 - 1))
+    tok_q2c = np.zeros((bsz, nch, c1 - 1))
+    mass = np.zeros((bsz, nch, hq, lqm))
     for b in range(bsz):
         for n in range(nch):
             for h in range(hq):
@@ -118,11 +132,15 @@ def prefill_ref(q_pre, k_pre, v_pre, q_qm, k_qm, v_qm, q_len, scale=None):
                 o[b, n, :, h, :] = u["o"]
                 lse[b, n, h] = u["lse"]
                 tok[b, n] += u["e_head"]
+                tok_q2c[b, n] += u["e_q2c_head"]
+                mass[b, n, h] = u["content_mass"]
     return {
         "o": o,
         "k_cache": cache_ref(k_pre),
         "v_cache": cache_ref(v_pre),
         "tok_score": tok,
+        "tok_score_q2c": tok_q2c,
         "key_mean": key_mean_ref(k_pre),
         "lse": lse,
+        "content_mass": mass,
     }

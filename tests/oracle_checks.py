@@ -25,6 +25,7 @@ import numpy as np
 import scipy.special
 import torch
 
+import oracle.chunk_score as OCS
 import oracle.decode as OD
 import oracle.prefill as OP
 import oracle.select as OS
@@ -75,6 +76,10 @@ def check_prefill_golden():
                             0, 0, 0, g["dims"]["L_q"], g["dims"]["scale"])
     want_p = np.array([[_frac(v) for v in row] for row in g["expect_probs"]])
     np.testing.assert_allclose(u["p"], want_p, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(r["content_mass"][0, 0, 0], [_frac(v) for v in g["expect_content_mass"]], atol=1e-12)
+    np.testing.assert_allclose(r["tok_score_q2c"][0, 0], [_frac(v) for v in g["expect_tok_score_q2c"]], atol=1e-12)
+    np.testing.assert_allclose(OCS.prefill_chunk_score_ref(r["content_mass"], g["dims"]["L_q"])[0, 0],
+                               np.log(_frac(g["expect_chunk_score_exp"])), atol=1e-12)
 
 
 def check_prefill_blockdiag_bruteforce(seed, per_chunk=False):
@@ -288,6 +293,99 @@ def check_token_rank(seed):
     for bt in (1, 4, 9):
         want = np.stack([np.stack([1 + OS.topk_ref(e[b, n], bt) for n in ci[b]]) for b in range(2)])
         assert np.array_equal(OS.tokens_by_rank_ref(r, ci, bt), want)
+
+
+# ----------------------------------------------------------------------------- prefill-time chunk score
+
+def check_chunk_score_golden():
+    """Two heads with different content masses (head average before the log), and
+    selection of the K lowest / highest given scores with a tie."""
+    g = _load("chunk_score_worked_example.json")
+    x = {k: np.array(g[k], dtype=np.float64) for k in ("q_pre", "k_pre", "v_pre", "q_qm", "k_qm", "v_qm")}
+    r = _prefill(x, g["dims"]["L_q"], g["dims"]["scale"])
+    want_mass = np.array([[_frac(v) for v in row] for row in g["expect_content_mass"]])
+    np.testing.assert_allclose(r["content_mass"][0, 0], want_mass, atol=1e-12)
+    np.testing.assert_allclose(r["tok_score"][0, 0], [_frac(v) for v in g["expect_tok_score"]], atol=1e-12)
+    np.testing.assert_allclose(r["tok_score_q2c"][0, 0], [_frac(v) for v in g["expect_tok_score_q2c"]], atol=1e-12)
+    s = OCS.prefill_chunk_score_ref(r["content_mass"], g["dims"]["L_q"])
+    np.testing.assert_allclose(s[0, 0], np.log(_frac(g["expect_chunk_score_exp"])), atol=1e-12)
+    sel = g["select"]
+    for case in sel["cases"]:
+        ci, ts = OCS.select_ranked_ref(np.array(sel["chunk_score"], float), np.array(sel["tok_rank"]),
+                                       case["top_k"], sel["tok_budget"], bool(case["lowest"]))
+        assert ci.tolist() == case["chunk_idx"], case
+        assert ts.tolist() == case["tok_slot"], case
+
+
+def check_chunk_score_uniform(seed, m_len):
+    """All queries zero: every row is uniform over the S_c columns, so each q/m row
+    puts C/S_c on the content and s = -ln(C/S_c) per non-empty term."""
+    x = tiny_prefill_inputs(seed, Lq=3, Lm=m_len, C=7)
+    x["q_pre"][:] = 0
+    x["q_qm"][:] = 0
+    r = _prefill(x, 3)
+    sc = 1 + 7 + 3 + m_len
+    np.testing.assert_allclose(r["content_mass"], 7 / sc, atol=1e-13)
+    terms = 2 if m_len > 0 else 1
+    np.testing.assert_allclose(OCS.prefill_chunk_score_ref(r["content_mass"], 3), -terms * np.log(7 / sc),
+                               atol=1e-12)
+
+
+def check_chunk_score_bruteforce(seed):
+    """Against the dense block-diagonal forward of all chunks at once (scipy
+    softmax over the concatenated sequences with -inf across chunks): the mass of
+    every q/m row on its own chunk's content columns, then the score written out
+    row by row with explicit loops."""
+    B, N, C, Lq, Lm, Hq, Hkv, d = 1, 3, 5, 2, 3, 4, 2, 8
+    x = tiny_prefill_inputs(seed, B, N, C, Lq, Lm, Hq, Hkv, d)
+    r = _prefill(x, Lq)
+    sc = 1 + C + Lq + Lm
+    scale = 1 / np.sqrt(d)
+    for h in range(Hq):
+        g = h // (Hq // Hkv)
+        qs = np.concatenate([np.concatenate([x["q_pre"][0, n, :, h], x["q_qm"][0, :, h]]) for n in range(N)])
+        ks = np.concatenate([np.concatenate([x["k_pre"][0, n, :, g], x["k_qm"][0, :, g]]) for n in range(N)])
+        logits = scale * qs @ ks.T
+        for n in range(N):
+            for m in range(N):
+                if m != n:
+                    logits[n * sc:(n + 1) * sc, m * sc:(m + 1) * sc] = -np.inf
+        p = scipy.special.softmax(logits, axis=1)
+        for n in range(N):
+            for i in range(Lq + Lm):
+                row = n * sc + 1 + C + i
+                np.testing.assert_allclose(r["content_mass"][0, n, h, i], p[row, n * sc + 1:n * sc + 1 + C].sum(),
+                                           atol=1e-13)
+    got = OCS.prefill_chunk_score_ref(r["content_mass"], Lq)
+    for n in range(N):
+        want = 0.0
+        for i in range(Lq + Lm):
+            a = sum(r["content_mass"][0, n, h, i] for h in range(Hq)) / Hq
+            want -= np.log(a) / (Lq if i < Lq else Lm)
+        np.testing.assert_allclose(got[0, n], want, atol=1e-12)
+
+
+def check_select_ranked_bruteforce(seed):
+    """Among all size-k subsets exactly one has every member ranking before every
+    non-member (score ascending, index ascending); selection of the K lowest returns
+    it, and the K highest is the K lowest of the negated scores."""
+    rng = np.random.default_rng(seed)
+    for trial in range(20):
+        n = int(rng.integers(1, 7))
+        x = rng.integers(-2, 3, size=(1, n)).astype(np.float64)
+        rank = np.stack([rng.permutation(4) for _ in range(n)])[None]
+        for k in range(1, n + 1):
+            def before(i, j):
+                return x[0, i] < x[0, j] or (x[0, i] == x[0, j] and i < j)
+            good = [c for c in itertools.combinations(range(n), k)
+                    if all(before(i, j) for i in c for j in range(n) if j not in c)]
+            assert len(good) == 1
+            ci, ts = OCS.select_ranked_ref(x, rank, k, 2, lowest=True)
+            assert ci[0].tolist() == list(good[0])
+            for kk, c in enumerate(good[0]):
+                assert ts[0, kk].tolist() == [1 + j for j in range(4) if rank[0, c, j] < 2]
+            hi, _ = OCS.select_ranked_ref(-x, rank, k, 2, lowest=False)
+            assert np.array_equal(hi, ci)
 
 
 # ----------------------------------------------------------------------------- stage (c)

@@ -7,6 +7,7 @@ only if every pin listed for it raises.
 import numpy as np
 import pytest
 
+import oracle.chunk_score as OCS
 import oracle.decode as OD
 import oracle.prefill as OP
 import oracle.select as OS
@@ -118,6 +119,43 @@ def _gather_no_bos(x_cache, chunk_idx, tok_slot):
     return np.stack(out)
 
 
+def _unit_mass_with_bos(*a, **k):
+    u = _orig_unit(*a, **k)
+    c1 = a[0].shape[2]
+    u["content_mass"] = u["p"][c1:, :c1].sum(axis=1)
+    return u
+
+
+def _unit_q2c_both(*a, **k):
+    u = _orig_unit(*a, **k)
+    u["e_q2c_head"] = u["e_head"]
+    return u
+
+
+def _score_mean_of_logs(content_mass, q_len):
+    nll = -np.log(np.asarray(content_mass, np.float64))          # per head
+    s_i = nll[..., :q_len].mean(axis=-1)
+    s_p = nll[..., q_len:].mean(axis=-1) if nll.shape[-1] > q_len else 0 * s_i
+    return (s_i + s_p).mean(axis=2)
+
+
+def _score_one_normaliser(content_mass, q_len):
+    a = np.asarray(content_mass, np.float64).mean(axis=2)
+    return -np.log(a).mean(axis=-1)
+
+
+def _score_no_pseudo_labels(content_mass, q_len):
+    a = np.asarray(content_mass, np.float64).mean(axis=2)
+    return -np.log(a[..., :q_len]).mean(axis=-1)
+
+
+_orig_select_ranked = OCS.select_ranked_ref
+
+
+def _select_ranked_ignores_order(chunk_score, tok_rank, top_k, tok_budget, lowest=True):
+    return _orig_select_ranked(chunk_score, tok_rank, top_k, tok_budget, lowest=False)
+
+
 MUTANTS = [
     ("softmax over columns", OP, "chunk_probs", _softmax_cols,
      [C.check_prefill_golden, lambda: C.check_prefill_sdpa(3)]),
@@ -150,6 +188,19 @@ MUTANTS = [
     ("gather drops the chunk BOS rows", OT, "gather_selected_ref", _gather_no_bos,
      [C.check_static_golden, lambda: C.check_gather_matches_decode_rows(1),
       lambda: C.check_compact_decode_equals_gathered(7, 3)]),
+    ("content mass includes the BOS column", OP, "prefill_unit_ref", _unit_mass_with_bos,
+     [C.check_prefill_golden, C.check_chunk_score_golden, lambda: C.check_chunk_score_uniform(21, 4),
+      lambda: C.check_chunk_score_bruteforce(22)]),
+    ("query-to-chunk score keeps both sums", OP, "prefill_unit_ref", _unit_q2c_both,
+     [C.check_prefill_golden, C.check_chunk_score_golden]),
+    ("chunk score averages the logs over heads", OCS, "prefill_chunk_score_ref", _score_mean_of_logs,
+     [C.check_chunk_score_golden, lambda: C.check_chunk_score_bruteforce(22)]),
+    ("chunk score uses one length for both terms", OCS, "prefill_chunk_score_ref", _score_one_normaliser,
+     [C.check_prefill_golden, C.check_chunk_score_golden, lambda: C.check_chunk_score_uniform(21, 4)]),
+    ("chunk score drops the pseudo-label term", OCS, "prefill_chunk_score_ref", _score_no_pseudo_labels,
+     [C.check_prefill_golden, C.check_chunk_score_golden, lambda: C.check_chunk_score_uniform(21, 4)]),
+    ("selection keeps the highest scores", OCS, "select_ranked_ref", _select_ranked_ignores_order,
+     [C.check_chunk_score_golden, lambda: C.check_select_ranked_bruteforce(24)]),
 ]
 
 

@@ -93,3 +93,21 @@ def test_compact_decode_equals_gathered(n_static):
 
 def test_compact_decode_sdpa():
     C.check_compact_decode_sdpa(5)
+
+
+def test_chunk_score_golden():
+    C.check_chunk_score_golden()
+
+
+@pytest.mark.parametrize("m_len", [0, 4])
+def test_chunk_score_uniform(m_len):
+    C.check_chunk_score_uniform(21, m_len)
+
+
+@pytest.mark.parametrize("seed", [22, 23])
+def test_chunk_score_bruteforce(seed):
+    C.check_chunk_score_bruteforce(seed)
+
+
+def test_select_ranked_bruteforce():
+    C.check_select_ranked_bruteforce(24)
