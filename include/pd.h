@@ -72,6 +72,10 @@ typedef struct {
                            [B][N][L_q+L_m][H][d]                                    */
   int32_t out_fp32;     /* 0: o and o_dec have element type dtype; 1: they are fp32
                            (bf16 inputs, fp32 outputs: no output rounding)          */
+  int32_t tok_score_dir; /* token score of pd_prefill_chunks: 0 = both sums of
+                           Eq. 5 (default); 1 = its first sum only, the mass the
+                           query rows put on the token (the query-to-chunk score
+                           of the paper's retention-score ablation)                 */
 } pd_dims;
 
 /*
@@ -96,11 +100,19 @@ typedef struct {
  *             (BOS at slot 0), chunk-contiguous per KV head
  *   tok_score fp32 [B][N][C]  e(c_j) of Eq. 5: for content token j, the
  *             softmax mass the L_q query rows put on it plus the mass it puts
- *             on the L_q query columns, summed over all H_q heads
+ *             on the L_q query columns, summed over all H_q heads (the first
+ *             term alone when dims->tok_score_dir = 1)
  *   tok_rank  int32 [B][N][C]  rank of token j among the C tokens of its chunk
  *             by tok_score: 0 = highest, ties to the lower index (Section 5.2:
  *             tokens are ranked by eviction score)
  *   key_mean  fp32 [B][N][H_kv][d]  mean of the C content keys (BOS excluded)
+ *   chunk_score fp32 [B][N] or NULL  prefill-time chunk score, lower = more
+ *             relevant: an attention-space reading of the length-normalised
+ *             NLLs s_I + s_P of Section 5.1 (Eqs. 3-4).  With a(r) the mass
+ *             q/m row r puts on the chunk's C content columns, averaged over
+ *             the H_q heads: s = -(1/L_q) sum_{query rows} ln a(r)
+ *             - (1/L_m) sum_{pseudo-label rows} ln a(r) (second term only when
+ *             L_m >= 1).  Select with pd_select_ranked(lowest = 1).
  * workspace: >= pd_workspace_bytes(dims, 0, 0, 0, 0) bytes.
  * Errors: PD_ERR_BAD_DIMS for a size out of range; see the status list.
  */
@@ -108,8 +120,23 @@ pd_status pd_prefill_chunks(const pd_dims *dims,
                             const void *q_pre, const void *k_pre, const void *v_pre,
                             const void *q_qm, const void *k_qm, const void *v_qm,
                             void *o, void *k_cache, void *v_cache,
-                            float *tok_score, int32_t *tok_rank, float *key_mean,
+                            float *tok_score, int32_t *tok_rank, float *key_mean, float *chunk_score,
                             void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * Stage (b) from given chunk scores (Section 5.2, inter-chunk sparsity: keep
+ * the K chunks with the lowest combined score), e.g. the chunk_score of
+ * pd_prefill_chunks, selected once before the denoising loop.
+ * Keeps the top_k lowest (lowest = 1) or highest (lowest = 0) of
+ * chunk_score fp32 [B][N] (ties to the lower index; -0 equals +0), and the
+ * tokens of each kept chunk with rank < tok_budget in tok_rank int32
+ * [B][N][C].  Outputs as pd_score_select: chunk_idx int32 [B][top_k]
+ * ascending; tok_slot int32 [B][top_k][tok_budget] ascending slots in 1..C.
+ * Sizes: 1 <= top_k <= N, 1 <= tok_budget <= C.  No workspace.
+ */
+pd_status pd_select_ranked(const pd_dims *dims, int32_t top_k, int32_t tok_budget, const float *chunk_score,
+                           int32_t lowest, const int32_t *tok_rank, int32_t *chunk_idx, int32_t *tok_slot,
+                           void *stream);
 
 /*
  * Stage (b), one layer, one denoising step: chunk scores, top-K chunks

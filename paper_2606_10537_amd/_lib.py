@@ -20,7 +20,7 @@ STATUS = {0: "PD_OK", 1: "PD_ERR_NULL_PTR", 2: "PD_ERR_BAD_DIMS", 3: "PD_ERR_UNS
 EXPORTS = ["pd_prefill_chunks", "pd_score_select", "pd_sparse_decode_attn", "pd_cache_bytes",
            "pd_workspace_bytes", "pd_decode_splits", "pd_status_string", "pd_last_error_message",
            "pd_version", "pd_mfma_rate_probe", "pd_score_select_static", "pd_gather_selected",
-           "pd_sparse_decode_attn_compact", "pd_compact_workspace_bytes"]
+           "pd_sparse_decode_attn_compact", "pd_compact_workspace_bytes", "pd_select_ranked"]
 
 
 class PdError(RuntimeError):
@@ -35,7 +35,7 @@ class PdDims(ctypes.Structure):
         ("q_len", ctypes.c_int32), ("m_len", ctypes.c_int32), ("dec_len", ctypes.c_int32),
         ("n_heads_q", ctypes.c_int32), ("n_heads_kv", ctypes.c_int32), ("head_dim", ctypes.c_int32),
         ("dtype", ctypes.c_int32), ("sm_scale", ctypes.c_float), ("qm_per_chunk", ctypes.c_int32),
-        ("out_fp32", ctypes.c_int32),
+        ("out_fp32", ctypes.c_int32), ("tok_score_dir", ctypes.c_int32),
     ]
 
 
@@ -55,6 +55,7 @@ class Dims:
     sm_scale: float = 0.0
     qm_per_chunk: int = 0
     out_fp32: int = 0
+    tok_score_dir: int = 0
 
     @property
     def seq_len(self):
@@ -64,7 +65,7 @@ class Dims:
     def c(self):
         return PdDims(self.batch, self.n_chunks, self.chunk_len, self.q_len, self.m_len, self.dec_len,
                       self.n_heads_q, self.n_heads_kv, self.head_dim, self.dtype, self.sm_scale,
-                      self.qm_per_chunk, self.out_fp32)
+                      self.qm_per_chunk, self.out_fp32, self.tok_score_dir)
 
 
 _lib = None
@@ -84,7 +85,7 @@ def load(path: str = LIB_PATH):
     lib = ctypes.CDLL(path)
     vp, sz, i32, fp = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_void_p
     dp = ctypes.POINTER(PdDims)
-    lib.pd_prefill_chunks.argtypes = [dp] + [vp] * 12 + [vp, sz, vp]
+    lib.pd_prefill_chunks.argtypes = [dp] + [vp] * 13 + [vp, sz, vp]
     lib.pd_prefill_chunks.restype = ctypes.c_int
     lib.pd_score_select.argtypes = [dp, i32, i32, vp, fp, fp, vp, vp, fp, vp, sz, vp]
     lib.pd_score_select.restype = ctypes.c_int
@@ -100,6 +101,8 @@ def load(path: str = LIB_PATH):
     lib.pd_status_string.restype = ctypes.c_char_p
     lib.pd_last_error_message.argtypes = []
     lib.pd_last_error_message.restype = ctypes.c_char_p
+    lib.pd_select_ranked.argtypes = [dp, i32, i32, fp, i32, fp, vp, vp, vp]
+    lib.pd_select_ranked.restype = ctypes.c_int
     lib.pd_score_select_static.argtypes = [dp, i32, i32, vp, fp, fp, vp, vp, fp, vp, sz, vp]
     lib.pd_score_select_static.restype = ctypes.c_int
     lib.pd_gather_selected.argtypes = [dp, i32, i32] + [vp] * 6 + [vp]
@@ -156,12 +159,20 @@ def pd_decode_splits(dims: Dims, top_k, tok_budget, n_static, num_splits=0) -> i
 
 
 def pd_prefill_chunks(dims: Dims, q_pre, k_pre, v_pre, q_qm, k_qm, v_qm, o, k_cache, v_cache,
-                      tok_score, tok_rank, key_mean, workspace, stream=None):
-    """Stage (a) for one layer (see include/pd.h)."""
+                      tok_score, tok_rank, key_mean, workspace, stream=None, chunk_score=None):
+    """Stage (a) for one layer (see include/pd.h); chunk_score (B, N) fp32 or None."""
     _check(load().pd_prefill_chunks(
         ctypes.byref(dims.c()), _ptr(q_pre), _ptr(k_pre), _ptr(v_pre), _ptr(q_qm), _ptr(k_qm), _ptr(v_qm),
         _ptr(o), _ptr(k_cache), _ptr(v_cache), _ptr(tok_score), _ptr(tok_rank), _ptr(key_mean),
-        _ptr(workspace), _nbytes(workspace), _stream(stream)))
+        _ptr(chunk_score), _ptr(workspace), _nbytes(workspace), _stream(stream)))
+
+
+def pd_select_ranked(dims: Dims, top_k, tok_budget, chunk_score, lowest, tok_rank, chunk_idx, tok_slot,
+                     stream=None):
+    """Top-K chunks by given scores (the lowest when lowest=1) and their kept tokens (see include/pd.h)."""
+    _check(load().pd_select_ranked(
+        ctypes.byref(dims.c()), top_k, tok_budget, _ptr(chunk_score), int(lowest), _ptr(tok_rank),
+        _ptr(chunk_idx), _ptr(tok_slot), _stream(stream)))
 
 
 def pd_score_select(dims: Dims, top_k, tok_budget, q_dec, key_mean, tok_rank, chunk_idx, tok_slot,

@@ -92,7 +92,17 @@ struct WaveState {
   float m;      // running row max (log2 domain), shared by lanes l and l^32
   float l;      // this lane's partial sum of the bf16-rounded weights that multiply V
   float lx;     // this lane's partial sum of the unrounded weights (prefill only)
-  float qmass;  // this lane's partial mass on the query columns (prefill only)
+  float qmass;  // this lane's partial mass on its counted key range (prefill only)
+};
+
+// Keys counted into qmass (prefill only), tile-relative: a lane whose query row
+// lies below `split` (row index within the wave's first row group; +32 per
+// further group) counts [lo0, hi0), the other lanes [lo1, hi1).  The prefill
+// counts the query columns for the BOS and content rows (Eq. 5, first sum)
+// and the content columns for the query and pseudo-label rows (the
+// prefill-time chunk score).
+struct MassRange {
+  int split, lo0, hi0, lo1, hi1;
 };
 
 // Lane-constant parts of the LDS fragment addresses (elements).  Everything
@@ -116,9 +126,8 @@ struct FragAddr {
 // One KV tile for one wave, in three phases: S^T = K Q^T (s_phase), online
 // softmax producing the bf16 weights P (softmax_phase), O^T += V^T P^T
 // (pv_phase).  kv_valid: number of valid keys in this tile (64 except in a
-// ragged last tile).  qlo/qhi: key range (tile-relative) counted into qmass;
-// empty when qlo >= qhi.  EXACT: also keep the unrounded row sum and the
-// query-column mass (prefill).  O is normalised by the sum of the same
+// ragged last tile).  mr: keys counted into qmass.  EXACT: also keep the
+// unrounded row sum and the counted mass (prefill).  O is normalised by the sum of the same
 // bf16-rounded weights that multiply V, so rounding P perturbs a convex
 // combination instead of scaling O.
 template <int D>
@@ -214,11 +223,12 @@ __device__ __forceinline__ float softmax_max(WaveState<D>& st, f32x16 (&s)[2], i
 }
 
 // Part 2 (branch-free): weights p, packed to bf16 in pk; s keeps the fp32 p
-// for the query-column mass.  The rounded weights' sum goes into l (one
-// v_dot2c_f32_bf16 with (1, 1) per packed pair), the exact sum into lx.
+// for the counted mass.  The rounded weights' sum goes into l (one
+// v_dot2c_f32_bf16 with (1, 1) per packed pair), the exact sum into lx; the
+// exact sum of this tile is returned.
 template <int D, bool EXACT>
-__device__ __forceinline__ void softmax_exp(WaveState<D>& st, f32x16 (&s)[2], uint32_t (&pk)[16], float nm,
-                                            float scale_log2) {
+__device__ __forceinline__ float softmax_exp(WaveState<D>& st, f32x16 (&s)[2], uint32_t (&pk)[16], float nm,
+                                             float scale_log2) {
   float lsum = 0.f;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
@@ -237,13 +247,23 @@ __device__ __forceinline__ void softmax_exp(WaveState<D>& st, f32x16 (&s)[2], ui
 #pragma unroll
   for (int i = 0; i < 16; ++i) lr = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[i]), ones, lr, false);
   st.l = lr;
+  return lsum;
 }
 
-// Part 3 (prefill only): mass of the keys qlo..qhi-1 (the query columns).
+// Part 3 (prefill only): mass of this lane's counted keys (row group h of the
+// wave).  A range covering the whole tile takes the tile's exact row sum; the
+// per-key test runs only in tiles where some lane's range is partial.
 template <int D>
-__device__ __forceinline__ void softmax_qmass(WaveState<D>& st, const f32x16 (&s)[2], int grp, int qlo, int qhi) {
-  if (qlo < qhi) {
-    float qs = 0.f;
+__device__ __forceinline__ void softmax_qmass(WaveState<D>& st, const f32x16 (&s)[2], int grp, int h,
+                                              const MassRange& mr, float lsum) {
+  if (mr.lo0 >= mr.hi0 && mr.lo1 >= mr.hi1) return;   // wave-uniform: nothing counted in this tile
+  const int l32 = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u)) & 31;   // lane % 32
+  const bool first = l32 + 32 * h < mr.split;
+  const int qlo = first ? mr.lo0 : mr.lo1, qhi = first ? mr.hi0 : mr.hi1;
+  const bool any = qlo < qhi;
+  float qs = lsum;
+  if (__ballot(any && (qlo > 0 || qhi < 64))) {
+    qs = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -251,16 +271,16 @@ __device__ __forceinline__ void softmax_qmass(WaveState<D>& st, const f32x16 (&s
         const int key = 32 * kb + 8 * (r >> 2) + 4 * grp + (r & 3);
         qs += (key >= qlo && key < qhi) ? s[kb][r] : 0.f;
       }
-    st.qmass += qs;
   }
+  st.qmass += any ? qs : 0.f;
 }
 
 template <int D, bool EXACT>
-__device__ __forceinline__ void softmax_phase(WaveState<D>& st, f32x16 (&s)[2], uint32_t (&pk)[16], int grp,
-                                              float scale_log2, int kv_valid, int qlo, int qhi) {
+__device__ __forceinline__ void softmax_phase(WaveState<D>& st, f32x16 (&s)[2], uint32_t (&pk)[16], int grp, int h,
+                                              float scale_log2, int kv_valid, const MassRange& mr) {
   const float nm = softmax_max<D, EXACT>(st, s, grp, scale_log2, kv_valid);
-  softmax_exp<D, EXACT>(st, s, pk, nm, scale_log2);
-  if constexpr (EXACT) softmax_qmass<D>(st, s, grp, qlo, qhi);
+  const float lsum = softmax_exp<D, EXACT>(st, s, pk, nm, scale_log2);
+  if constexpr (EXACT) softmax_qmass<D>(st, s, grp, h, mr, lsum);
 }
 
 // V^T fragment of k-step kk and d block db (two transposing reads).
@@ -308,13 +328,13 @@ __device__ __forceinline__ void pv_phase(WaveState<D> (&st)[NH], const uint32_t 
 template <int D, int NH, bool EXACT>
 __device__ __forceinline__ void wave_step(WaveState<D> (&st)[NH], uint32_t (&pk)[NH][16], bool deferred, bool first,
                                           bool last, const uint16_t* Ks, const uint16_t* Vs, const uint16_t* Vs_prev,
-                                          const FragAddr& fa, int grp, float scale_log2, int kv_valid, int qlo,
-                                          int qhi) {
+                                          const FragAddr& fa, int grp, float scale_log2, int kv_valid,
+                                          const MassRange& mr) {
   f32x16 s[NH][2];
   if (deferred && !first) pv_phase<D, NH>(st, pk, Vs_prev, fa);
   s_phase<D, NH>(s, st, Ks, fa);
 #pragma unroll
-  for (int h = 0; h < NH; ++h) softmax_phase<D, EXACT>(st[h], s[h], pk[h], grp, scale_log2, kv_valid, qlo, qhi);
+  for (int h = 0; h < NH; ++h) softmax_phase<D, EXACT>(st[h], s[h], pk[h], grp, h, scale_log2, kv_valid, mr);
   if (!deferred || last) pv_phase<D, NH>(st, pk, Vs, fa);
 }
 
@@ -433,10 +453,11 @@ __device__ __forceinline__ void kv_sweep(uint16_t* const* Kb, uint16_t* const* V
 }
 
 // ---------------------------------------------------------------------------
-// Stage (a): chunk prefill.  Workgroup = (b, n, h, 128-row query tile).
+// Stage (a): chunk prefill.  Workgroup = (b, n, h, 256-row query tile).
 // Also writes the chunk KV cache (each KV tile by exactly one workgroup of the
-// (b, n, kv-head) group), the per-head query-column mass of the content rows
-// and the log2-domain LSE of the query rows.
+// (b, n, kv-head) group), the per-head query-column mass of the content rows,
+// the log2-domain LSE of the query rows and, when asked, the per-head
+// content mass of the query and pseudo-label rows.
 template <int D>
 __global__ __launch_bounds__(Tile<D>::NT, 1) void prefill_bf16_kernel(PrefillArgs p) {
   using T = Tile<D>;
@@ -514,6 +535,8 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void prefill_bf16_kernel(PrefillArg
   };
 
   const int qc_lo = C1, qc_hi = C1 + p.Lq;   // query columns counted by Eq. 5
+  const int cm_hi = p.qm_mass ? C1 : 1;       // content columns counted for the chunk score (if asked)
+  const int split = C1 - (qt * T::BM + wave * T::NH * 32);
   uint32_t pk_prev[T::NH][16];
   const bool deferred = wave_group(wave) != 0;
   kv_sweep<D>(Kb, Vb, 0, p.n_kvt, dma, cache_write,
@@ -521,9 +544,10 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void prefill_bf16_kernel(PrefillArg
                 if (!wave_active) return;
                 const int t0 = t * T::BN;
                 const int kv_valid = min(T::BN, p.Sc - t0);
-                const int lo = max(qc_lo - t0, 0), hi = min(qc_hi - t0, T::BN);
+                const MassRange mr{split, max(qc_lo - t0, 0), min(qc_hi - t0, T::BN), max(1 - t0, 0),
+                                   min(cm_hi - t0, T::BN)};
                 wave_step<D, T::NH, true>(st, pk_prev, deferred, t == 0, last, ks, vs, vs_prev, fa, grp,
-                                          p.scale_log2, kv_valid, lo, hi);
+                                          p.scale_log2, kv_valid, mr);
               });
   if (!wave_active) return;
 
@@ -542,6 +566,7 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void prefill_bf16_kernel(PrefillArg
         const size_t hb = chunk * p.Hq + h;
         if (qrow >= 1 && qrow < C1) p.part_i[hb * p.C + (qrow - 1)] = qtot / lxtot;
         if (qrow >= qc_lo && qrow < qc_hi) p.lse_q[hb * p.Lq + (qrow - qc_lo)] = st[j].m + __log2f(lxtot);
+        if (p.qm_mass && qrow >= C1) p.qm_mass[hb * (p.Lq + p.Lm) + (qrow - C1)] = qtot / lxtot;
       }
     }
   }
@@ -662,7 +687,7 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void decode_bf16_kernel(DecodeArgs 
                 if (!wave_active) return;
                 const int kv_valid = min(T::BN, L_kv - t * T::BN);
                 wave_step<D, T::NH, false>(st, pk_prev, deferred, t == t_begin, last, ks, vs, vs_prev, fa, grp,
-                                           p.scale_log2, kv_valid, 0, 0);
+                                           p.scale_log2, kv_valid, MassRange{0, 0, 0, 0, 0});
               });
   if (!wave_active) return;
 
@@ -689,9 +714,10 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void decode_bf16_kernel(DecodeArgs 
 }
 
 // ---------------------------------------------------------------------------
-// Eq. 5, second sum: for each content token j, the softmax mass the L_q query
-// rows put on it, summed over heads, plus the first sum (per-head query-column
-// mass of row j, written by the prefill kernel).  Workgroup = (b, n, 64 content
+// Eq. 5, first sum: for each content token j, the softmax mass the L_q query
+// rows put on it, summed over heads, plus (unless only the query-to-chunk
+// direction is asked for) the second sum (per-head query-column mass of row j,
+// written by the prefill kernel).  Workgroup = (b, n, 64 content
 // columns); wave w handles heads w, w+4, ...  S = Q_q K_c^T on MFMA, then
 // exp2(S*scale - lse2(row)) with the query rows' final LSE from the prefill.
 template <int D>
@@ -759,7 +785,8 @@ __global__ __launch_bounds__(256) void escore_bf16_kernel(EscoreArgs p) {
     const int j = cb * 64 + tid;
     if (j < p.C) {
       float e = 0.f;
-      for (int h = 0; h < p.Hq; ++h) e += p.part_i[(chunk * p.Hq + h) * p.C + j];
+      if (!p.q2c)
+        for (int h = 0; h < p.Hq; ++h) e += p.part_i[(chunk * p.Hq + h) * p.C + j];
       e += ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
       p.tok_score[chunk * p.C + j] = e;
     }

@@ -1,4 +1,4 @@
-// fp32 attention kernels (stage a prefill, Eq. 5 second sum, stage c decode).
+// fp32 attention kernels (stage a prefill, Eq. 5 first sum, stage c decode).
 //
 // On MI355X the fp32 matrix-core peak equals the fp32 vector peak, so the fp32
 // path runs on plain VALU FMAs: one thread owns one query row (q and the
@@ -108,7 +108,12 @@ __global__ __launch_bounds__(64) void prefill_f32_kernel(PrefillArgs p) {
   else if (row < p.Sc) qsrc = q_qm + ((qm_base + (row - C1)) * p.Hq + h) * D;
   row_init<D>(st, qsrc);
 
+  // Keys counted into qmass: the query columns for the BOS and content rows
+  // (second sum of Eq. 5), the content columns for the query and pseudo-label
+  // rows when the chunk score is asked for.
   const int qc_lo = C1, qc_hi = C1 + p.Lq;
+  const int m_lo = row < C1 ? qc_lo : 1;
+  const int m_hi = row < C1 ? qc_hi : (p.qm_mass ? C1 : 1);
   const int ntile = (p.Sc + kF32Keys - 1) / kF32Keys;
   constexpr int CPR = D / 4;
   for (int t = 0; t < ntile; ++t) {
@@ -130,7 +135,7 @@ __global__ __launch_bounds__(64) void prefill_f32_kernel(PrefillArgs p) {
     }
     __syncthreads();
     const int t0 = t * kF32Keys;
-    row_tile<D>(st, Ks, Vs, min(kF32Keys, p.Sc - t0), p.scale_log2, qc_lo - t0, qc_hi - t0);
+    row_tile<D>(st, Ks, Vs, min(kF32Keys, p.Sc - t0), p.scale_log2, m_lo - t0, m_hi - t0);
     __syncthreads();
   }
   if (row >= p.Sc) return;
@@ -139,6 +144,7 @@ __global__ __launch_bounds__(64) void prefill_f32_kernel(PrefillArgs p) {
   const size_t hb = chunk * p.Hq + h;
   if (row >= 1 && row < C1) p.part_i[hb * p.C + (row - 1)] = st.qmass * inv;
   if (row >= qc_lo && row < qc_hi) p.lse_q[hb * p.Lq + (row - qc_lo)] = st.m + __log2f(st.l);
+  if (p.qm_mass && row >= C1) p.qm_mass[hb * (p.Lq + p.Lm) + (row - C1)] = st.qmass * inv;
 }
 
 // ---------------------------------------------------------------------------
@@ -192,7 +198,8 @@ __global__ __launch_bounds__(64) void escore_f32_kernel(EscoreArgs p) {
   }
   if (j < p.C) {
     float e = 0.f;
-    for (int h = 0; h < p.Hq; ++h) e += p.part_i[(chunk * p.Hq + h) * p.C + j];
+    if (!p.q2c)
+      for (int h = 0; h < p.Hq; ++h) e += p.part_i[(chunk * p.Hq + h) * p.C + j];
     p.tok_score[chunk * p.C + j] = e + acc;
   }
 }

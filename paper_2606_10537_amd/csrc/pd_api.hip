@@ -58,6 +58,8 @@ pd_status check_dims(const pd_dims* d) {
     return fail(PD_ERR_BAD_DIMS, "qm_per_chunk=%d must be 0 or 1", d->qm_per_chunk);
   if (d->out_fp32 != 0 && d->out_fp32 != 1)
     return fail(PD_ERR_BAD_DIMS, "out_fp32=%d must be 0 or 1", d->out_fp32);
+  if (d->tok_score_dir != 0 && d->tok_score_dir != 1)
+    return fail(PD_ERR_BAD_DIMS, "tok_score_dir=%d must be 0 or 1", d->tok_score_dir);
   if (d->n_heads_q % d->n_heads_kv != 0)
     return fail(PD_ERR_UNSUPPORTED, "n_heads_q=%d is not a multiple of n_heads_kv=%d", d->n_heads_q, d->n_heads_kv);
   if (d->head_dim != 64 && d->head_dim != 128)
@@ -86,14 +88,15 @@ float scale_of(const pd_dims* d) { return d->sm_scale > 0.f ? d->sm_scale : 1.0f
 
 // --- workspace layouts -------------------------------------------------------
 struct PrefillWs {
-  size_t part_i, lse_q, total;
+  size_t part_i, lse_q, qm_mass, total;
 };
 PrefillWs prefill_ws(const pd_dims* d) {
   PrefillWs w;
   const size_t bnh = (size_t)d->batch * d->n_chunks * d->n_heads_q;
   w.part_i = 0;
   w.lse_q = round_up(bnh * d->chunk_len * sizeof(float));
-  w.total = w.lse_q + round_up(bnh * d->q_len * sizeof(float));
+  w.qm_mass = w.lse_q + round_up(bnh * d->q_len * sizeof(float));
+  w.total = w.qm_mass + round_up(bnh * (d->q_len + d->m_len) * sizeof(float));
   return w;
 }
 
@@ -228,8 +231,8 @@ int32_t pd_decode_splits(const pd_dims* d, int32_t top_k, int32_t tok_budget, in
 
 pd_status pd_prefill_chunks(const pd_dims* d, const void* q_pre, const void* k_pre, const void* v_pre,
                             const void* q_qm, const void* k_qm, const void* v_qm, void* o, void* k_cache,
-                            void* v_cache, float* tok_score, int32_t* tok_rank, float* key_mean, void* workspace,
-                            size_t ws_bytes, void* stream) {
+                            void* v_cache, float* tok_score, int32_t* tok_rank, float* key_mean, float* chunk_score,
+                            void* workspace, size_t ws_bytes, void* stream) {
   PD_RETURN_IF(check_dims(d));
   PD_REQUIRE_PTR(q_pre);
   PD_REQUIRE_PTR(k_pre);
@@ -243,6 +246,8 @@ pd_status pd_prefill_chunks(const pd_dims* d, const void* q_pre, const void* k_p
   PD_REQUIRE_PTR(tok_score);
   PD_REQUIRE_PTR(tok_rank);
   PD_REQUIRE_PTR(key_mean);
+  if (chunk_score && !aligned16(chunk_score))
+    return fail(PD_ERR_MISALIGNED, "pointer 'chunk_score' is not 16-byte aligned");
   const PrefillWs w = prefill_ws(d);
   PD_RETURN_IF(check_ws(workspace, ws_bytes, w.total));
 
@@ -261,6 +266,7 @@ pd_status pd_prefill_chunks(const pd_dims* d, const void* q_pre, const void* k_p
   a.v_cache = (uint16_t*)v_cache;
   a.part_i = (float*)(ws + w.part_i);
   a.lse_q = (float*)(ws + w.lse_q);
+  a.qm_mass = chunk_score ? (float*)(ws + w.qm_mass) : nullptr;
   a.B = d->batch;
   a.N = d->n_chunks;
   a.C = d->chunk_len;
@@ -294,6 +300,7 @@ pd_status pd_prefill_chunks(const pd_dims* d, const void* q_pre, const void* k_p
   e.n_cb = cdiv(a.C, 64);
   e.total = a.B * a.N * e.n_cb;
   e.qm_per_chunk = a.qm_per_chunk;
+  e.q2c = d->tok_score_dir;
   e.scale_log2 = a.scale_log2;
 
   hipError_t err;
@@ -312,8 +319,30 @@ pd_status pd_prefill_chunks(const pd_dims* d, const void* q_pre, const void* k_p
   }
   err = pd::launch_token_rank(tok_score, tok_rank, a.B, a.N, a.C, s);
   if (err != hipSuccess) return hip_status(err, "token-rank kernel");
+  if (chunk_score) {
+    err = pd::launch_chunk_score(a.qm_mass, chunk_score, a.B, a.N, a.Hq, a.Lq, a.Lm, s);
+    if (err != hipSuccess) return hip_status(err, "chunk-score kernel");
+  }
   err = pd::launch_key_mean(k_cache, key_mean, a.B, a.N, a.C, a.Hkv, d->head_dim, bf16, s);
   return hip_status(err, "key-mean kernel");
+}
+
+pd_status pd_select_ranked(const pd_dims* d, int32_t top_k, int32_t tok_budget, const float* chunk_score,
+                           int32_t lowest, const int32_t* tok_rank, int32_t* chunk_idx, int32_t* tok_slot,
+                           void* stream) {
+  PD_RETURN_IF(check_dims(d));
+  if (top_k < 1 || top_k > d->n_chunks)
+    return fail(PD_ERR_BAD_DIMS, "top_k=%d must be in 1..n_chunks=%d", top_k, d->n_chunks);
+  if (tok_budget < 1 || tok_budget > d->chunk_len)
+    return fail(PD_ERR_BAD_DIMS, "tok_budget=%d must be in 1..chunk_len=%d", tok_budget, d->chunk_len);
+  if (lowest != 0 && lowest != 1) return fail(PD_ERR_BAD_DIMS, "lowest=%d must be 0 or 1", lowest);
+  PD_REQUIRE_PTR(chunk_score);
+  PD_REQUIRE_PTR(tok_rank);
+  PD_REQUIRE_PTR(chunk_idx);
+  PD_REQUIRE_PTR(tok_slot);
+  return hip_status(pd::launch_select_ranked(chunk_score, lowest, tok_rank, chunk_idx, tok_slot, d->batch,
+                                             d->n_chunks, d->chunk_len, top_k, tok_budget, (hipStream_t)stream),
+                    "select kernel");
 }
 
 pd_status pd_score_select(const pd_dims* d, int32_t top_k, int32_t tok_budget, const void* q_dec,

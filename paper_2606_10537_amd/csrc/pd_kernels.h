@@ -35,6 +35,7 @@ struct PrefillArgs {
   uint16_t *o, *k_cache, *v_cache;
   float* part_i;   // [B][N][Hq][C]  per-head mass of content row j on the query columns
   float* lse_q;    // [B][N][Hq][Lq] log2-domain LSE of the query rows
+  float* qm_mass;  // [B][N][Hq][Lq+Lm] mass of each q/m row on the C content columns, or nullptr
   int B, N, C, Lq, Lm, Hq, Hkv, G, Sc;
   int n_qt, n_kvt, total;
   int qm_per_chunk;
@@ -47,6 +48,7 @@ struct EscoreArgs {
   const float *part_i, *lse_q;
   float* tok_score;
   int B, N, C, Lq, Lm, Hq, Hkv, G, n_cb, total, qm_per_chunk;
+  int q2c;           // 1: only the query rows' mass on the token (query-to-chunk score)
   float scale_log2;
 };
 
@@ -102,6 +104,10 @@ hipError_t launch_gather_selected(const void* k_cache, const void* v_cache, cons
                                   int K, int Bt, int row_bytes, hipStream_t s);
 hipError_t launch_mfma_rate(int n_workgroups, int iters, float* sink, hipStream_t s);
 hipError_t launch_token_rank(const float* tok_score, int32_t* tok_rank, int B, int N, int C, hipStream_t s);
+hipError_t launch_chunk_score(const float* qm_mass, float* chunk_score, int B, int N, int Hq, int Lq, int Lm,
+                              hipStream_t s);
+hipError_t launch_select_ranked(const float* chunk_score, int lowest, const int32_t* tok_rank, int32_t* chunk_idx,
+                                int32_t* tok_slot, int B, int N, int C, int K, int Bt, hipStream_t s);
 int select_row_splits(int Ld);
 
 }  // namespace pd

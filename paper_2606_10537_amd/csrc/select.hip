@@ -10,6 +10,8 @@
 //                                  key means of that head's KV group;
 //   gather:     grid (rows)     -- static-selection mode: kept rows copied once
 //                                  into a contiguous per-(sequence, KV head) buffer;
+//   chunk_score: grid (b, n)    -- prefill-time chunk score from the content
+//                                  mass of the query and pseudo-label rows;
 //   select:     grid (b, k)     -- sums the terms of every chunk in a fixed
 //                                  order, ranks the N scores (bitonic sort in
 //                                  LDS), takes the k-th kept chunk in ascending
@@ -170,9 +172,10 @@ __global__ __launch_bounds__(256) void qscore_kernel(const void* q_dec, const fl
   }
 }
 
+// neg = 1 keeps the K lowest scores instead of the K highest.
 __global__ __launch_bounds__(256) void select_kernel(const float* partial, const int32_t* tok_rank,
                                                       float* chunk_score, int32_t* chunk_idx, int32_t* tok_slot,
-                                                      int N, int C, int K, int Bt, int T, int Npad) {
+                                                      int N, int C, int K, int Bt, int T, int Npad, int neg) {
   extern __shared__ __attribute__((aligned(16))) uint64_t keys[];
   __shared__ int my_chunk;
   __shared__ int scan[2][256];
@@ -197,7 +200,7 @@ __global__ __launch_bounds__(256) void select_kernel(const float* partial, const
       s += __shfl_xor(s, 2);
       s += __shfl_xor(s, 4);
       if (j == 0 && n < N) {
-        keys[n] = rank_key(s, n);
+        keys[n] = rank_key(neg ? -s : s, n);
         if (k == 0 && chunk_score) chunk_score[(size_t)b * N + n] = s;
       }
     }
@@ -251,7 +254,54 @@ hipError_t launch_score_select(const SelectArgs& a, hipStream_t s) {
   if (err != hipSuccess) return err;
   const int Npad = next_pow2(a.N);
   hipLaunchKernelGGL(select_kernel, dim3(a.B * a.K), dim3(256), (size_t)Npad * 8, s, a.partial, a.tok_rank,
-                     a.chunk_score, a.chunk_idx, a.tok_slot, a.N, a.C, a.K, a.Bt, a.Hq * a.NS, Npad);
+                     a.chunk_score, a.chunk_idx, a.tok_slot, a.N, a.C, a.K, a.Bt, a.Hq * a.NS, Npad, 0);
+  return hipGetLastError();
+}
+
+// Selection from scores the caller supplies (one term per chunk).
+hipError_t launch_select_ranked(const float* chunk_score, int lowest, const int32_t* tok_rank, int32_t* chunk_idx,
+                                int32_t* tok_slot, int B, int N, int C, int K, int Bt, hipStream_t s) {
+  const int Npad = next_pow2(N);
+  hipLaunchKernelGGL(select_kernel, dim3(B * K), dim3(256), (size_t)Npad * 8, s, chunk_score, tok_rank,
+                     (float*)nullptr, chunk_idx, tok_slot, N, C, K, Bt, 1, Npad, lowest);
+  return hipGetLastError();
+}
+
+// Prefill-time chunk score of one (b, n) from the per-head content masses of
+// its L_q + L_m query and pseudo-label rows: a(r) = (1/H_q) sum_h mass[h][r],
+// s = -(1/L_q) sum_{r < L_q} ln a(r) - (1/L_m) sum_{r >= L_q} ln a(r) (the
+// second term only when L_m > 0).  Thread t takes rows t, t + 256, ...; both
+// sums are reduced by a fixed tree, so the result is reproducible.
+__global__ __launch_bounds__(256) void chunk_score_kernel(const float* qm_mass, float* chunk_score, int Hq, int Lq,
+                                                           int Lm) {
+  __shared__ float red[2][256];
+  const size_t bn = blockIdx.x;
+  const int R = Lq + Lm, t = threadIdx.x;
+  const float* m = qm_mass + bn * Hq * R;
+  float si = 0.f, sp = 0.f;
+  for (int r = t; r < R; r += 256) {
+    float a = 0.f;
+    for (int h = 0; h < Hq; ++h) a += m[(size_t)h * R + r];
+    const float nl = -logf(a / Hq);
+    if (r < Lq) si += nl;
+    else sp += nl;
+  }
+  red[0][t] = si;
+  red[1][t] = sp;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (t < w) {
+      red[0][t] += red[0][t + w];
+      red[1][t] += red[1][t + w];
+    }
+    __syncthreads();
+  }
+  if (t == 0) chunk_score[bn] = red[0][0] / Lq + (Lm > 0 ? red[1][0] / Lm : 0.f);
+}
+
+hipError_t launch_chunk_score(const float* qm_mass, float* chunk_score, int B, int N, int Hq, int Lq, int Lm,
+                              hipStream_t s) {
+  hipLaunchKernelGGL(chunk_score_kernel, dim3(B * N), dim3(256), 0, s, qm_mass, chunk_score, Hq, Lq, Lm);
   return hipGetLastError();
 }
 

@@ -24,7 +24,7 @@ def workspace(nbytes, device="cuda"):
     return torch.empty(max(nbytes, 16), dtype=torch.uint8, device=device)
 
 
-def run_prefill(d: Dims, x, stream=None):
+def run_prefill(d: Dims, x, stream=None, chunk_score=False):
     dev, dt = x["q_pre"].device, x["q_pre"].dtype
     B, N, C, Hq, Hkv, D = d.batch, d.n_chunks, d.chunk_len, d.n_heads_q, d.n_heads_kv, d.head_dim
     odt = torch.float32 if d.out_fp32 else dt
@@ -36,11 +36,12 @@ def run_prefill(d: Dims, x, stream=None):
         "tok_rank": torch.full((B, N, C), -1, dtype=torch.int32, device=dev),
         "key_mean": torch.full((B, N, Hkv, D), float("nan"), dtype=torch.float32, device=dev),
     }
+    if chunk_score:
+        out["chunk_score"] = torch.full((B, N), float("nan"), dtype=torch.float32, device=dev)
     ws = workspace(_lib.pd_workspace_bytes(d, which=0), dev)
     _lib.pd_prefill_chunks(d, x["q_pre"], x["k_pre"], x["v_pre"], x["q_qm"], x["k_qm"], x["v_qm"],
                            out["o"], out["k_cache"], out["v_cache"], out["tok_score"], out["tok_rank"],
-                           out["key_mean"], ws,
-                           stream)
+                           out["key_mean"], ws, stream, chunk_score=out.get("chunk_score"))
     return out
 
 

@@ -53,7 +53,7 @@ def dims(**kw):
 
 def prefill(d, ws=A, wsn=1 << 30, **ptrs):
     names = ["q_pre", "k_pre", "v_pre", "q_qm", "k_qm", "v_qm", "o", "k_cache", "v_cache", "tok_score", "tok_rank",
-             "key_mean"]
+             "key_mean", "chunk_score"]
     args = [ptrs.get(n, A) for n in names]
     lib = _lib.load()
     dd = d.c() if d is not None else None
@@ -80,6 +80,8 @@ def test_prefill_validation(lib):
     assert prefill(dims(), ws=None) == 5
     assert prefill(dims(), wsn=16) == 5
     assert prefill(dims(), ws=MIS) == 4
+    assert prefill(dims(tok_score_dir=2)) == 2
+    assert prefill(dims(), chunk_score=MIS) == 4
 
 
 def test_select_validation(lib):
@@ -146,6 +148,20 @@ def test_static_mode_validation(lib):
     assert _lib.pd_compact_workspace_bytes(d, 100, 3) >= 3 * 1 * 4 * 32 * 65 * 4
 
 
+def test_select_ranked_validation(lib):
+    c = ctypes.byref(dims().c())
+    call = lambda k=2, bt=64, cs=A, low=1, tr=A, ci=A, dd=c: lib.pd_select_ranked(dd, k, bt, cs, low, tr, ci, A, None)
+    assert call(dd=None) == 1
+    assert call(k=0) == 2
+    assert call(k=5) == 2            # top_k > N
+    assert call(bt=129) == 2         # tok_budget > C
+    assert call(low=2) == 2
+    assert call(cs=None) == 1
+    assert call(tr=None) == 1
+    assert call(ci=MIS) == 4
+    assert call(dd=ctypes.byref(dims(tok_score_dir=-1).c())) == 2
+
+
 def test_mfma_probe_validation(lib):
     assert lib.pd_mfma_rate_probe(0, 10, A, None) == 2
     assert lib.pd_mfma_rate_probe(4, 0, A, None) == 2
@@ -159,7 +175,7 @@ def test_size_queries():
     d32 = dims(dtype=PD_FP32)
     assert _lib.pd_cache_bytes(d32) == 1 * 4 * 4 * 129 * 64 * 4
     assert _lib.pd_workspace_bytes(dims(batch=0), 0, 0, 0, 0) == 0
-    assert _lib.pd_workspace_bytes(d, 0, 0, 0, 0) >= 2 * 3 * 4 * (100 + 16) * 4
+    assert _lib.pd_workspace_bytes(d, 0, 0, 0, 0) >= 2 * 3 * 4 * (100 + 16 + 16 + 32) * 4
     # One shard needs no decode workspace; S shards need S partial outputs.
     assert _lib.pd_workspace_bytes(d, 2, 50, 1, 2) == 0
     assert _lib.pd_workspace_bytes(d, 2, 50, 3, 2) >= 3 * 2 * 4 * 32 * 129 * 4
