@@ -39,9 +39,9 @@ def parse():
                    help="write this many MiB before every decode launch, so that each launch starts with the "
                         "last-level cache (MALL) holding none of its operands (cold numbers)")
     p.add_argument("--no-static", action="store_true",
-                   help="skip the static-selection-mode measurement after the timed region")
+                   help="skip the static-selection and prefill-score schedule measurements after the timed region")
     p.add_argument("--no-achievable", action="store_true",
-                   help="skip the achievable-peak measurements (library GEMM, device copy) after the timed region")
+                   help="skip the achievable-peak measurements (MFMA-rate diagnostic, device copy) after the timed region")
     p.add_argument("--calib-copy-mib", type=int, default=0,
                    help="before timing, copy this many MiB once (a plain copy kernel of known size for "
                         "calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -198,11 +198,60 @@ def static_mode(torch, _lib, w, d, pool, dec_pool, k_cache, v_cache, key_mean, t
     launch_ms = sum(a.elapsed_time(b) for a, b in ev) / len(ev)
     return {"steps_per_s": round(T / (loop_ms * 1e-3), 3),
             "job_steps_per_s": round(T / ((pre_ms_layer * L + sg_ms + loop_ms) * 1e-3), 3),
+            "loop_ms": round(loop_ms, 3),
             "select_gather_ms_per_layer": round(sg_ms / L, 4),
             "decode_launch_ms": round(launch_ms, 5),
             "decode_tflops": round(dec_flop / (launch_ms * 1e-3) / 1e12, 2),
             "note": "selection once per layer from the pseudo-label rows, kept rows compacted once; decode over "
                     "the compact buffer; same caches, decode inputs and flop count as the per-step mode"}
+
+
+def prefill_score_mode(torch, _lib, w, d, pool, prefill_bufs, k_cache, v_cache, tok_rank, key_mean, stream,
+                       static_loop_ms):
+    """The paper's own schedule with the prefill-time chunk score, measured after the timed region:
+    every layer's prefill also writes the chunk scores, the K lowest chunks are kept and their kept
+    rows compacted once; the T-step loop of compact decodes is the one static_mode timed (same kernels,
+    sizes and decode inputs; decode time does not depend on which rows were kept)."""
+    dev = "cuda"
+    L, T, K, Bt = w.layers, w.steps, w.top_k, w.tok_budget
+    B, Hkv, D = w.batch, w.n_heads_kv, w.head_dim
+    n_sel = K * (1 + Bt)
+    sh = stream.cuda_stream
+    o_pre, tok_score, ws_pre = prefill_bufs
+    cs = torch.empty((B, w.n_chunks), dtype=torch.float32, device=dev)
+    ci = torch.empty((B, K), dtype=torch.int32, device=dev)
+    ts = torch.empty((B, K, Bt), dtype=torch.int32, device=dev)
+    k_sel = torch.empty((B, Hkv, n_sel, D), dtype=w.torch_dtype, device=dev)
+    v_sel = torch.empty_like(k_sel)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(L)]
+
+    def run(record):
+        for l in range(L):
+            x = pool[l % len(pool)]
+            if record:
+                ev[l][0].record(stream)
+            _lib.pd_prefill_chunks(d, x["q_pre"], x["k_pre"], x["v_pre"], x["q_qm"], x["k_qm"], x["v_qm"], o_pre,
+                                   k_cache[l], v_cache[l], tok_score, tok_rank[l], key_mean[l], ws_pre, sh,
+                                   chunk_score=cs)
+            if record:
+                ev[l][1].record(stream)
+            _lib.pd_select_ranked(d, K, Bt, cs, 1, tok_rank[l], ci, ts, sh)
+            _lib.pd_gather_selected(d, K, Bt, k_cache[l], v_cache[l], ci, ts, k_sel, v_sel, sh)
+            if record:
+                ev[l][2].record(stream)
+
+    run(False)
+    torch.cuda.synchronize()
+    run(True)
+    torch.cuda.synchronize()
+    pre = sum(a.elapsed_time(b) for a, b, _ in ev) / L
+    sel = sum(b.elapsed_time(c) for _, b, c in ev) / L
+    return {"prefill_ms_per_layer": round(pre, 3),
+            "select_gather_ms_per_layer": round(sel, 4),
+            "job_steps_per_s": round(T / (((pre + sel) * L + static_loop_ms) * 1e-3), 3),
+            "note": "prefill also writes the chunk scores (attention mass of the query and pseudo-label rows on "
+                    "each chunk's content); the K lowest kept once per layer, kept rows compacted; decode loop "
+                    "as in static_mode"}
 
 
 def achievable_peaks(torch, dev):
@@ -389,6 +438,9 @@ def main():
     if not args.no_static:
         res["static_mode"] = static_mode(torch, _lib, w, d, pool, dec_pool, k_cache, v_cache, key_mean, tok_rank,
                                          stream, dec_flop, pre_ms_layer, n_static)
+        res["prefill_score_mode"] = prefill_score_mode(torch, _lib, w, d, pool, (o_pre, tok_score, ws_pre),
+                                                       k_cache, v_cache, tok_rank, key_mean, stream,
+                                                       res["static_mode"]["loop_ms"])
     if not args.no_achievable:
         ach = achievable_peaks(torch, dev)
         res["achievable"] = ach

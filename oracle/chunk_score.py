@@ -20,6 +20,11 @@ mass it puts on the chunk's content in the same forward:
 
 a_h comes from ``oracle.prefill`` (``content_mass``).  Ties in the selection
 rank the lower chunk index first; the kept lists are ascending.
+
+Pinned by: a hand-derived two-head example, the one-head prefill example, the
+closed form for all-zero queries, the dense block-diagonal forward of all
+chunks, and subset enumeration for the K lowest.  Against the paper itself
+the score is parity unpinned: the paper prints no value of this reading.
 """
 
 import numpy as np

@@ -16,6 +16,10 @@ Ties rank the lower index first for chunks and tokens alike, and both lists
 are returned in ascending order.  Token lists hold cache slots 1..C (slot 0 is
 the chunk's BOS row, which every kept chunk contributes on top of the B
 tokens).
+
+The chunk score is pinned to the definition above (worked example, zero
+query, linearity, GQA group mapping); against the paper it is parity
+unpinned: the paper prints no value of this proxy.
 """
 
 import numpy as np
