@@ -23,6 +23,8 @@ that each step can be checked against the paper by eye:
 * ``chunk_score`` -- the prefill-time chunk score built from the attention
   mass the query and pseudo-label rows put on the chunk content (an
   attention-space reading of Eqs. 3-4), and selection of the K lowest.
+* ``full_mask`` -- full-mask cache construction: the kept rows and the query
+  rows rotated to continuous positions and encoded jointly.
 
 Parity status of each function is stated in its docstring ("pinned by ...").
 """
@@ -45,6 +47,7 @@ from .static import (
     decode_compact_ref,
 )
 from .chunk_score import prefill_chunk_score_ref, select_ranked_ref
+from .full_mask import rope_rotate_ref, joint_deltas, joint_rows_ref, joint_attention_ref
 
 __all__ = [
     "chunk_rows",
@@ -68,4 +71,8 @@ __all__ = [
     "decode_compact_ref",
     "prefill_chunk_score_ref",
     "select_ranked_ref",
+    "rope_rotate_ref",
+    "joint_deltas",
+    "joint_rows_ref",
+    "joint_attention_ref",
 ]

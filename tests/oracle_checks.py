@@ -27,6 +27,7 @@ import torch
 
 import oracle.chunk_score as OCS
 import oracle.decode as OD
+import oracle.full_mask as OF
 import oracle.prefill as OP
 import oracle.select as OS
 import oracle.static as OT
@@ -386,6 +387,126 @@ def check_select_ranked_bruteforce(seed):
                 assert ts[0, kk].tolist() == [1 + j for j in range(4) if rank[0, c, j] < 2]
             hi, _ = OCS.select_ranked_ref(-x, rank, k, 2, lowest=False)
             assert np.array_equal(hi, ci)
+
+
+# ----------------------------------------------------------------------------- full-mask construction
+
+def _mathexpr(e):
+    import math
+    return float(eval(e, {"__builtins__": {}}, {"sin": math.sin, "cos": math.cos}))
+
+
+def check_full_mask_golden():
+    g = _load("full_mask_worked_example.json")
+    for case in g["rope"]:
+        got = OF.rope_rotate_ref(np.array(case["x"], float), case["delta"], case["base"])
+        np.testing.assert_allclose(got, [_mathexpr(e) for e in case["expect"]], atol=1e-14)
+    dl = g["deltas"]
+    assert OF.joint_deltas(dl["K"], dl["B"], dl["L_q"], dl["C"]).tolist() == dl["expect"]
+
+
+def _rope_complex(u, pos, base):
+    """Rotary embedding of u at absolute position pos, as complex multiplication of the
+    rotate-half pairs (u_i + i u_{i+d/2}) by exp(i pos theta_i)."""
+    d = u.shape[-1]
+    half = d // 2
+    theta = float(base) ** (-2.0 * np.arange(half) / d)
+    z = (u[..., :half] + 1j * u[..., half:]) * np.exp(1j * np.asarray(pos, float)[..., None] * theta)
+    return np.concatenate([z.real, z.imag], axis=-1)
+
+
+def check_rope_composition(seed):
+    """Re-rotating a row embedded at its chunk-local position p by delta equals embedding
+    it at p + delta directly; moving by delta then by -delta is the identity; a common
+    move leaves every q.k unchanged (scores see relative positions only)."""
+    rng = np.random.default_rng(seed)
+    u = rng.standard_normal((5, 16))
+    p = rng.integers(0, 50, size=5)
+    delta = rng.integers(0, 5000, size=5)
+    for base in (10000.0, 1e6):
+        local = _rope_complex(u, p, base)
+        np.testing.assert_allclose(OF.rope_rotate_ref(local, delta, base), _rope_complex(u, p + delta, base),
+                                   atol=1e-9)
+        np.testing.assert_allclose(OF.rope_rotate_ref(OF.rope_rotate_ref(local, delta, base), -delta, base), local,
+                                   atol=1e-9)
+        q = rng.standard_normal(16)
+        k = rng.standard_normal(16)
+        np.testing.assert_allclose(OF.rope_rotate_ref(q, 1234, base) @ OF.rope_rotate_ref(k, 1234, base), q @ k,
+                                   atol=1e-10)
+    assert np.array_equal(OF.rope_rotate_ref(u, delta, 0), u)
+
+
+def _tiny_full_mask(seed, B=2, N=4, C=6, Lq=3, Lm=2, Hq=4, Hkv=2, d=8, K=2, Bt=3):
+    x = tiny_prefill_inputs(seed, B, N, C, Lq, Lm, Hq, Hkv, d)
+    ci, ts = _tiny_selection(seed + 1, B, N, C, K, Bt)
+    kc = OP.cache_ref(x["k_pre"])
+    vc = OP.cache_ref(x["v_pre"])
+    return x, kc, vc, ci, ts
+
+
+def check_joint_rows(seed):
+    """Joint rows without rotation: the kept cache rows in decode order (the same rows
+    the static-mode gather copies), then the query rows; with rotation the values stay
+    put and Q, K move by the per-row deltas."""
+    x, kc, vc, ci, ts = _tiny_full_mask(seed)
+    Lq = 3
+    q, k, v = OF.joint_rows_ref(x["q_pre"], kc, vc, x["q_qm"], x["k_qm"], x["v_qm"], ci, ts, Lq, 0)
+    n_sel = ci.shape[1] * (1 + ts.shape[2])
+    np.testing.assert_array_equal(np.transpose(k[:, :n_sel], (0, 2, 1, 3)), OT.gather_selected_ref(kc, ci, ts))
+    np.testing.assert_array_equal(np.transpose(v[:, :n_sel], (0, 2, 1, 3)), OT.gather_selected_ref(vc, ci, ts))
+    np.testing.assert_array_equal(k[:, n_sel:], x["k_qm"][:, :Lq])
+    for b in range(2):
+        for kk in range(ci.shape[1]):
+            n = ci[b, kk]
+            np.testing.assert_array_equal(q[b, kk * (1 + ts.shape[2])], x["q_pre"][b, n, 0])
+    q2, k2, v2 = OF.joint_rows_ref(x["q_pre"], kc, vc, x["q_qm"], x["k_qm"], x["v_qm"], ci, ts, Lq, 10000.0)
+    np.testing.assert_array_equal(v2, v)
+    deltas = OF.joint_deltas(ci.shape[1], ts.shape[2], Lq, 6)
+    np.testing.assert_allclose(k2, _rope_complex_moved(k, deltas), atol=1e-9)
+    np.testing.assert_allclose(q2, _rope_complex_moved(q, deltas), atol=1e-9)
+
+
+def _rope_complex_moved(x, deltas, base=10000.0):
+    """Move rows (B, L, H, d) by deltas (L,) with the complex-number rotation."""
+    d = x.shape[-1]
+    half = d // 2
+    theta = base ** (-2.0 * np.arange(half) / d)
+    z = (x[..., :half] + 1j * x[..., half:]) * np.exp(1j * deltas[None, :, None, None] * theta)
+    return np.concatenate([z.real, z.imag], axis=-1)
+
+
+def check_joint_attention_sdpa(seed):
+    """The joint pass against torch scaled_dot_product_attention (float64, CPU, no mask)."""
+    x, kc, vc, ci, ts = _tiny_full_mask(seed)
+    q, k, v = OF.joint_rows_ref(x["q_pre"], kc, vc, x["q_qm"], x["k_qm"], x["v_qm"], ci, ts, 3, 10000.0)
+    o, lse = OF.joint_attention_ref(q, k, v)
+    G = q.shape[2] // k.shape[2]
+    qt = torch.from_numpy(q).permute(0, 2, 1, 3)
+    kt = torch.from_numpy(np.repeat(k, G, axis=2)).permute(0, 2, 1, 3).contiguous()
+    vt = torch.from_numpy(np.repeat(v, G, axis=2)).permute(0, 2, 1, 3).contiguous()
+    want = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt).permute(0, 2, 1, 3).numpy()
+    np.testing.assert_allclose(o, want, atol=1e-12)
+    s = torch.einsum("bhqd,bhkd->bhqk", qt, kt) / np.sqrt(q.shape[-1])
+    np.testing.assert_allclose(lse, torch.logsumexp(s, dim=-1).numpy(), atol=1e-12)
+
+
+def check_full_mask_dense(seed):
+    """Everything kept (K = N, B = C) and no rotation: the joint pass is dense attention
+    over all chunk rows (BOS included) followed by the query rows, built here by explicit
+    concatenation."""
+    B, N, C, Lq, Hq, Hkv, d = 1, 3, 4, 2, 2, 1, 8
+    x = tiny_prefill_inputs(seed, B, N, C, Lq, 1, Hq, Hkv, d)
+    ci = np.arange(N)[None]
+    ts = np.tile(np.arange(1, C + 1), (1, N, 1))
+    q, k, v = OF.joint_rows_ref(x["q_pre"], OP.cache_ref(x["k_pre"]), OP.cache_ref(x["v_pre"]), x["q_qm"], x["k_qm"],
+                                x["v_qm"], ci, ts, Lq, 0)
+    o, _ = OF.joint_attention_ref(q, k, v)
+    for h in range(Hq):
+        qa = np.concatenate([x["q_pre"][0, n, :, h] for n in range(N)] + [x["q_qm"][0, :Lq, h]])
+        ka = np.concatenate([x["k_pre"][0, n, :, 0] for n in range(N)] + [x["k_qm"][0, :Lq, 0]])
+        va = np.concatenate([x["v_pre"][0, n, :, 0] for n in range(N)] + [x["v_qm"][0, :Lq, 0]])
+        p = scipy.special.softmax(qa @ ka.T / np.sqrt(d), axis=1)
+        np.testing.assert_allclose(o[0, :, h], p @ va, atol=1e-12)
 
 
 # ----------------------------------------------------------------------------- stage (c)

@@ -9,6 +9,7 @@ import pytest
 
 import oracle.chunk_score as OCS
 import oracle.decode as OD
+import oracle.full_mask as OF
 import oracle.prefill as OP
 import oracle.select as OS
 import oracle.static as OT
@@ -156,6 +157,57 @@ def _select_ranked_ignores_order(chunk_score, tok_rank, top_k, tok_budget, lowes
     return _orig_select_ranked(chunk_score, tok_rank, top_k, tok_budget, lowest=False)
 
 
+_orig_rope = OF.rope_rotate_ref
+_orig_joint_rows = OF.joint_rows_ref
+
+
+def _rope_interleaved(x, delta, base):
+    x = np.asarray(x, np.float64)
+    if base == 0:
+        return x.copy()
+    d = x.shape[-1]
+    out = np.empty_like(x)
+    delta = np.asarray(delta, np.float64)
+    for i in range(d // 2):
+        ang = delta * float(base) ** (-2.0 * i / d)
+        a, b = x[..., 2 * i], x[..., 2 * i + 1]
+        out[..., 2 * i] = a * np.cos(ang) - b * np.sin(ang)
+        out[..., 2 * i + 1] = b * np.cos(ang) + a * np.sin(ang)
+    return out
+
+
+def _rope_wrong_frequency(x, delta, base):
+    x = np.asarray(x, np.float64)
+    if base == 0:
+        return x.copy()
+    d = x.shape[-1]
+    half = d // 2
+    out = np.empty_like(x)
+    delta = np.asarray(delta, np.float64)
+    for i in range(half):
+        ang = delta * float(base) ** (-1.0 * i / d)
+        a, b = x[..., i], x[..., i + half]
+        out[..., i] = a * np.cos(ang) - b * np.sin(ang)
+        out[..., i + half] = b * np.cos(ang) + a * np.sin(ang)
+    return out
+
+
+def _rope_backwards(x, delta, base):
+    return _orig_rope(x, -np.asarray(delta, np.float64), base)
+
+
+def _deltas_query_one_chunk_late(top_k, tok_budget, q_len, chunk_len):
+    c1 = chunk_len + 1
+    return np.array([k * c1 for k in range(top_k) for _ in range(1 + tok_budget)] + [top_k * c1] * q_len, float)
+
+
+def _joint_rows_values_rotated(*a, **k):
+    q, kk, v = _orig_joint_rows(*a, **k)
+    ci, ts, q_len, base = a[6], a[7], a[8], a[9]
+    deltas = OF.joint_deltas(np.asarray(ts).shape[1], np.asarray(ts).shape[2], q_len, np.asarray(a[1]).shape[3] - 1)
+    return q, kk, _orig_rope(v, deltas[None, :, None], base)
+
+
 MUTANTS = [
     ("softmax over columns", OP, "chunk_probs", _softmax_cols,
      [C.check_prefill_golden, lambda: C.check_prefill_sdpa(3)]),
@@ -201,6 +253,16 @@ MUTANTS = [
      [C.check_prefill_golden, C.check_chunk_score_golden, lambda: C.check_chunk_score_uniform(21, 4)]),
     ("selection keeps the highest scores", OCS, "select_ranked_ref", _select_ranked_ignores_order,
      [C.check_chunk_score_golden, lambda: C.check_select_ranked_bruteforce(24)]),
+    ("rotary pairs interleaved", OF, "rope_rotate_ref", _rope_interleaved,
+     [C.check_full_mask_golden, lambda: C.check_rope_composition(31), lambda: C.check_joint_rows(32)]),
+    ("rotary frequency exponent halved", OF, "rope_rotate_ref", _rope_wrong_frequency,
+     [C.check_full_mask_golden, lambda: C.check_rope_composition(31)]),
+    ("rows moved backwards", OF, "rope_rotate_ref", _rope_backwards,
+     [C.check_full_mask_golden, lambda: C.check_rope_composition(31), lambda: C.check_joint_rows(32)]),
+    ("query rows placed one chunk late", OF, "joint_deltas", _deltas_query_one_chunk_late,
+     [C.check_full_mask_golden]),
+    ("values rotated with the keys", OF, "joint_rows_ref", _joint_rows_values_rotated,
+     [lambda: C.check_joint_rows(32)]),
 ]
 
 

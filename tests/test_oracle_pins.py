@@ -111,3 +111,24 @@ def test_chunk_score_bruteforce(seed):
 
 def test_select_ranked_bruteforce():
     C.check_select_ranked_bruteforce(24)
+
+
+def test_full_mask_golden():
+    C.check_full_mask_golden()
+
+
+def test_rope_composition():
+    C.check_rope_composition(31)
+
+
+@pytest.mark.parametrize("seed", [32, 33])
+def test_joint_rows(seed):
+    C.check_joint_rows(seed)
+
+
+def test_joint_attention_sdpa():
+    C.check_joint_attention_sdpa(34)
+
+
+def test_full_mask_dense():
+    C.check_full_mask_dense(35)
