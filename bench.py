@@ -254,6 +254,90 @@ def prefill_score_mode(torch, _lib, w, d, pool, prefill_bufs, k_cache, v_cache, 
                     "as in static_mode"}
 
 
+def full_mask_mode(torch, _lib, w, d, pool, dec_pool, prefill_bufs, k_cache, v_cache, tok_rank, key_mean, stream,
+                   rope_base=500000.0):
+    """Full-mask cache construction, measured after the timed region: per layer the prefill with the
+    chunk score, the K lowest chunks kept, their kept rows and the query rows moved to continuous
+    positions (rotary re-rotation) and attended densely together; then the T-step loop of compact
+    decodes whose prefix is the L_j joint rows (same row count as the static mode's prefix + static
+    rows, so the same decode flop count)."""
+    from paper_2606_10537_amd import synth
+    dev = "cuda"
+    L, T, K, Bt = w.layers, w.steps, w.top_k, w.tok_budget
+    B, Hq, Hkv, D = w.batch, w.n_heads_q, w.n_heads_kv, w.head_dim
+    Lj = K * (1 + Bt) + w.q_len
+    dj = synth.Workload(**{**w.__dict__, "dec_len": Lj}).dims()
+    sh = stream.cuda_stream
+    o_pre, tok_score, ws_pre = prefill_bufs
+    dt = w.torch_dtype
+    cs = torch.empty((B, w.n_chunks), dtype=torch.float32, device=dev)
+    ci = torch.empty((B, K), dtype=torch.int32, device=dev)
+    ts = torch.empty((B, K, Bt), dtype=torch.int32, device=dev)
+    qj = torch.empty((B, Lj, Hq, D), dtype=dt, device=dev)
+    kj, vj = torch.empty((B, Lj, Hkv, D), dtype=dt, device=dev), torch.empty((B, Lj, Hkv, D), dtype=dt, device=dev)
+    oj = torch.empty_like(qj)
+    kp = [torch.empty((B, Hkv, Lj, D), dtype=dt, device=dev) for _ in range(L)]
+    vp = [torch.empty_like(kp[0]) for _ in range(L)]
+    ws_joint = torch.empty(max(16, _lib.pd_compact_workspace_bytes(dj, 0, 0)), dtype=torch.uint8, device=dev)
+    ws_dec = torch.empty(max(16, _lib.pd_compact_workspace_bytes(d, Lj, 0)), dtype=torch.uint8, device=dev)
+    o_dec = torch.empty((B, w.dec_len, Hq, D), dtype=dt, device=dev)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(L)]
+    dec_slots = len(dec_pool[0])
+
+    def build(record):
+        for l in range(L):
+            x = pool[l % len(pool)]
+            if record:
+                ev[l][0].record(stream)
+            _lib.pd_prefill_chunks(d, x["q_pre"], x["k_pre"], x["v_pre"], x["q_qm"], x["k_qm"], x["v_qm"], o_pre,
+                                   k_cache[l], v_cache[l], tok_score, tok_rank[l], key_mean[l], ws_pre, sh,
+                                   chunk_score=cs)
+            if record:
+                ev[l][1].record(stream)
+            _lib.pd_select_ranked(d, K, Bt, cs, 1, tok_rank[l], ci, ts, sh)
+            if record:
+                ev[l][2].record(stream)
+            _lib.pd_gather_joint(d, K, Bt, ci, ts, x["q_pre"], k_cache[l], v_cache[l], x["q_qm"], x["k_qm"],
+                                 x["v_qm"], rope_base, qj, kj, vj, kp[l], vp[l], sh)
+            if record:
+                ev[l][3].record(stream)
+            _lib.pd_sparse_decode_attn_compact(dj, 0, qj, kj, vj, None, None, None, None, 0, oj, None, 0,
+                                               ws_joint, sh)
+            if record:
+                ev[l][4].record(stream)
+
+    def loop():
+        for t in range(T):
+            for l in range(L):
+                dd = dec_pool[l][t % dec_slots]
+                _lib.pd_sparse_decode_attn_compact(d, Lj, dd["q_dec"], dd["k_dec"], dd["v_dec"], kp[l], vp[l], None,
+                                                   None, 0, o_dec, None, 0, ws_dec, sh)
+
+    build(False)
+    loop()
+    torch.cuda.synchronize()
+    build(True)
+    s1, s2 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s1.record(stream)
+    loop()
+    s2.record(stream)
+    torch.cuda.synchronize()
+    per = [sum(e[i].elapsed_time(e[i + 1]) for e in ev) / L for i in range(4)]
+    loop_ms = s1.elapsed_time(s2)
+    joint_flop = 4.0 * B * Hq * Lj * Lj * D
+    return {"prefill_ms_per_layer": round(per[0], 3),
+            "select_ms_per_layer": round(per[1], 4),
+            "gather_joint_ms_per_layer": round(per[2], 4),
+            "joint_attn_ms_per_layer": round(per[3], 4),
+            "joint_attn_tflops": round(joint_flop / (per[3] * 1e-3) / 1e12, 2),
+            "loop_ms": round(loop_ms, 3),
+            "job_steps_per_s": round(T / ((sum(per) * L + loop_ms) * 1e-3), 3),
+            "joint_rows": Lj, "rope_base": rope_base,
+            "note": "prefill with the chunk score; K lowest kept; kept rows + query rows re-rotated to continuous "
+                    "positions and attended densely together (the one-layer slice of the joint re-encoding); "
+                    "decode loop over the L_j joint rows"}
+
+
 def achievable_peaks(torch, dev):
     """Achievable (not published) peaks on this GPU, measured after the timed region: the library's
     MFMA-rate diagnostic (register-only v_mfma_f32_32x32x16_bf16 chains on every CU) and a
@@ -441,6 +525,8 @@ def main():
         res["prefill_score_mode"] = prefill_score_mode(torch, _lib, w, d, pool, (o_pre, tok_score, ws_pre),
                                                        k_cache, v_cache, tok_rank, key_mean, stream,
                                                        res["static_mode"]["loop_ms"])
+        res["full_mask_mode"] = full_mask_mode(torch, _lib, w, d, pool, dec_pool, (o_pre, tok_score, ws_pre),
+                                               k_cache, v_cache, tok_rank, key_mean, stream)
     if not args.no_achievable:
         ach = achievable_peaks(torch, dev)
         res["achievable"] = ach

@@ -176,7 +176,7 @@ pd_status pd_score_select(const pd_dims *dims, int32_t top_k, int32_t tok_budget
  * Outputs: o_dec [B][L_d][H_q][d] (dtype, or fp32 when out_fp32 = 1);
  *   lse_dec fp32 [B][H_q][L_d] natural-log
  *   row LSE, or NULL (bf16 path: the log of the sum of
- *   the bf16-rounded softmax weights that multiply V, within log(1 + 2^-9)).
+ *   the bf16-rounded softmax weights that multiply V, within log(1 + 2^-8)).
  * num_splits: the KV rows are cut into that many shards processed in
  *   parallel and merged by log-sum-exp (the paper's Split-S); 0 = chosen by the
  *   library from the sizes; otherwise 1..64.
@@ -233,6 +233,53 @@ pd_status pd_sparse_decode_attn_compact(const pd_dims *dims, int32_t n_sel,
                                         void *o_dec, float *lse_dec, int32_t num_splits,
                                         void *workspace, size_t ws_bytes, void *stream);
 size_t pd_compact_workspace_bytes(const pd_dims *dims, int32_t n_sel, int32_t num_splits);
+
+/*
+ * Full-mask cache construction (Section 6, the ablation of the KV cache
+ * construction strategy): once the chunks are selected, the kept rows and the
+ * query are re-encoded jointly, with the decoding mask, at continuous
+ * positions.  pd_gather_joint builds the joint rows of every sequence; one
+ * pd_sparse_decode_attn_compact call over them (dims->dec_len = L_j,
+ * n_sel = 0, n_static = 0, k_sel / v_sel / k_static / v_static NULL, q_dec,
+ * k_dec, v_dec = q_joint, k_joint, v_joint) is the dense joint attention, and
+ * k_pref, v_pref (the same K, V rows in the compact prefix layout) then serve
+ * as the prefix (n_sel = L_j) of the decoding steps'
+ * pd_sparse_decode_attn_compact calls.
+ *
+ * Joint rows, L_j = top_k*(1+tok_budget) + L_q per sequence: for each kept
+ * chunk k = 0..top_k-1 (chunk_idx[b][k]) its BOS row (slot 0) and the rows at
+ * slots tok_slot[b][k][*]; then query rows 0..L_q-1 of the q/m block (layout
+ * per dims->qm_per_chunk, chunk 0's copy when per chunk).  Q rows come from
+ * q_pre, K and V rows from k_cache / v_cache (kept rows) or q_qm / k_qm / v_qm
+ * (query rows).
+ * Positions: the chunk forward placed slot s of every chunk at s and query row
+ * j at C+1+j; jointly, kept chunk k starts at k*(C+1), so its rows move by
+ * k*(C+1), and the query rows move by (top_k-1)*(C+1).  Q and K are rotated
+ * by the rotate-half rotary embedding with frequencies
+ * rope_base^(-2i/d), i = 0..d/2-1 (element i pairs with element i + d/2);
+ * the angle and the rotation are evaluated in double precision and rounded
+ * once to dims->dtype.  V is copied.  rope_base = 0: no rotation (bit-exact
+ * copies).
+ *
+ * Inputs (dims->dtype): q_pre [B][N][1+C][H_q][d] (as given to
+ *   pd_prefill_chunks); k_cache, v_cache as written by pd_prefill_chunks;
+ *   q_qm, k_qm, v_qm as given to pd_prefill_chunks; chunk_idx [B][top_k],
+ *   tok_slot [B][top_k][tok_budget] as written by the selection calls
+ *   (entries must lie in 0..N-1 and 1..C).
+ * Outputs (dims->dtype, caller-owned): q_joint [B][L_j][H_q][d], k_joint and
+ *   v_joint [B][L_j][H_kv][d]; k_pref and v_pref [B][H_kv][L_j][d], the same
+ *   K and V values (both NULL: not written; one NULL: PD_ERR_NULL_PTR).  No
+ *   workspace; asynchronous on stream.
+ * Sizes: 1 <= top_k <= N, 1 <= tok_budget <= C, rope_base finite and >= 0.
+ * Errors: PD_ERR_NULL_PTR, PD_ERR_MISALIGNED, PD_ERR_BAD_DIMS,
+ *   PD_ERR_UNSUPPORTED, PD_ERR_HIP.
+ */
+pd_status pd_gather_joint(const pd_dims *dims, int32_t top_k, int32_t tok_budget,
+                          const int32_t *chunk_idx, const int32_t *tok_slot,
+                          const void *q_pre, const void *k_cache, const void *v_cache,
+                          const void *q_qm, const void *k_qm, const void *v_qm, double rope_base,
+                          void *q_joint, void *k_joint, void *v_joint, void *k_pref, void *v_pref,
+                          void *stream);
 
 /* Bytes of ONE of k_cache / v_cache for one layer: B*N*H_kv*(1+C)*d*elem. */
 size_t pd_cache_bytes(const pd_dims *dims);

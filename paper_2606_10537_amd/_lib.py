@@ -20,7 +20,8 @@ STATUS = {0: "PD_OK", 1: "PD_ERR_NULL_PTR", 2: "PD_ERR_BAD_DIMS", 3: "PD_ERR_UNS
 EXPORTS = ["pd_prefill_chunks", "pd_score_select", "pd_sparse_decode_attn", "pd_cache_bytes",
            "pd_workspace_bytes", "pd_decode_splits", "pd_status_string", "pd_last_error_message",
            "pd_version", "pd_mfma_rate_probe", "pd_score_select_static", "pd_gather_selected",
-           "pd_sparse_decode_attn_compact", "pd_compact_workspace_bytes", "pd_select_ranked"]
+           "pd_sparse_decode_attn_compact", "pd_compact_workspace_bytes", "pd_select_ranked",
+           "pd_gather_joint"]
 
 
 class PdError(RuntimeError):
@@ -107,6 +108,8 @@ def load(path: str = LIB_PATH):
     lib.pd_score_select_static.restype = ctypes.c_int
     lib.pd_gather_selected.argtypes = [dp, i32, i32] + [vp] * 6 + [vp]
     lib.pd_gather_selected.restype = ctypes.c_int
+    lib.pd_gather_joint.argtypes = [dp, i32, i32] + [vp] * 8 + [ctypes.c_double] + [vp] * 6
+    lib.pd_gather_joint.restype = ctypes.c_int
     lib.pd_sparse_decode_attn_compact.argtypes = [dp, i32] + [vp] * 7 + [i32, vp, fp, i32, vp, sz, vp]
     lib.pd_sparse_decode_attn_compact.restype = ctypes.c_int
     lib.pd_compact_workspace_bytes.argtypes = [dp, i32, i32]
@@ -210,6 +213,15 @@ def pd_gather_selected(dims: Dims, top_k, tok_budget, k_cache, v_cache, chunk_id
     _check(load().pd_gather_selected(
         ctypes.byref(dims.c()), top_k, tok_budget, _ptr(k_cache), _ptr(v_cache), _ptr(chunk_idx),
         _ptr(tok_slot), _ptr(k_sel), _ptr(v_sel), _stream(stream)))
+
+
+def pd_gather_joint(dims: Dims, top_k, tok_budget, chunk_idx, tok_slot, q_pre, k_cache, v_cache, q_qm, k_qm,
+                    v_qm, rope_base, q_joint, k_joint, v_joint, k_pref=None, v_pref=None, stream=None):
+    """Full-mask mode: joint rows [kept rows ; query rows] at continuous positions (see include/pd.h)."""
+    _check(load().pd_gather_joint(
+        ctypes.byref(dims.c()), top_k, tok_budget, _ptr(chunk_idx), _ptr(tok_slot), _ptr(q_pre), _ptr(k_cache),
+        _ptr(v_cache), _ptr(q_qm), _ptr(k_qm), _ptr(v_qm), float(rope_base), _ptr(q_joint), _ptr(k_joint),
+        _ptr(v_joint), _ptr(k_pref), _ptr(v_pref), _stream(stream)))
 
 
 def pd_sparse_decode_attn_compact(dims: Dims, n_sel, q_dec, k_dec, v_dec, k_sel, v_sel, k_static, v_static,

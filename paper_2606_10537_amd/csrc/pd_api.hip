@@ -458,6 +458,68 @@ pd_status pd_gather_selected(const pd_dims* d, int32_t top_k, int32_t tok_budget
                     "gather kernel");
 }
 
+pd_status pd_gather_joint(const pd_dims* d, int32_t top_k, int32_t tok_budget, const int32_t* chunk_idx,
+                          const int32_t* tok_slot, const void* q_pre, const void* k_cache, const void* v_cache,
+                          const void* q_qm, const void* k_qm, const void* v_qm, double rope_base, void* q_joint,
+                          void* k_joint, void* v_joint, void* k_pref, void* v_pref, void* stream) {
+  PD_RETURN_IF(check_dims(d));
+  if (top_k < 1 || top_k > d->n_chunks)
+    return fail(PD_ERR_BAD_DIMS, "top_k=%d must be in 1..n_chunks=%d", top_k, d->n_chunks);
+  if (tok_budget < 1 || tok_budget > d->chunk_len)
+    return fail(PD_ERR_BAD_DIMS, "tok_budget=%d must be in 1..chunk_len=%d", tok_budget, d->chunk_len);
+  if (!std::isfinite(rope_base) || rope_base < 0.0)
+    return fail(PD_ERR_BAD_DIMS, "rope_base must be finite and >= 0 (0: no rotation)");
+  PD_REQUIRE_PTR(chunk_idx);
+  PD_REQUIRE_PTR(tok_slot);
+  PD_REQUIRE_PTR(q_pre);
+  PD_REQUIRE_PTR(k_cache);
+  PD_REQUIRE_PTR(v_cache);
+  PD_REQUIRE_PTR(q_qm);
+  PD_REQUIRE_PTR(k_qm);
+  PD_REQUIRE_PTR(v_qm);
+  PD_REQUIRE_PTR(q_joint);
+  PD_REQUIRE_PTR(k_joint);
+  PD_REQUIRE_PTR(v_joint);
+  if ((k_pref == nullptr) != (v_pref == nullptr))
+    return fail(PD_ERR_NULL_PTR, "k_pref and v_pref must be both given or both NULL");
+  if (k_pref && (!aligned16(k_pref) || !aligned16(v_pref)))
+    return fail(PD_ERR_MISALIGNED, "pointer 'k_pref' or 'v_pref' is not 16-byte aligned");
+  const long long lj = n_sel_of(top_k, tok_budget) + d->q_len;
+  if (lj * d->n_heads_q * d->head_dim >= (1LL << 31))
+    return fail(PD_ERR_BAD_DIMS, "joint rows of one sequence (L_j*n_heads_q*head_dim) must stay below 2^31 elements");
+  if ((long long)d->batch * lj >= (1LL << 31)) return fail(PD_ERR_BAD_DIMS, "batch*L_j must stay below 2^31");
+  pd::JointArgs a{};
+  a.q_pre = q_pre;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.q_qm = q_qm;
+  a.k_qm = k_qm;
+  a.v_qm = v_qm;
+  a.chunk_idx = chunk_idx;
+  a.tok_slot = tok_slot;
+  a.q_joint = q_joint;
+  a.k_joint = k_joint;
+  a.v_joint = v_joint;
+  a.k_pref = k_pref;
+  a.v_pref = v_pref;
+  a.B = d->batch;
+  a.N = d->n_chunks;
+  a.C = d->chunk_len;
+  a.Lq = d->q_len;
+  a.Lm = d->m_len;
+  a.Hq = d->n_heads_q;
+  a.Hkv = d->n_heads_kv;
+  a.G = a.Hq / a.Hkv;
+  a.D = d->head_dim;
+  a.K = top_k;
+  a.Bt = tok_budget;
+  a.Lj = (int)lj;
+  a.qm_per_chunk = d->qm_per_chunk;
+  a.elem_bytes = elem_bytes(d);
+  a.rope_base = rope_base;
+  return hip_status(pd::launch_gather_joint(a, (hipStream_t)stream), "joint gather kernel");
+}
+
 // Shared by the gathered and the compact decode entry points (arguments checked
 // by the caller except the common ones below).
 static pd_status decode_core(const pd_dims* d, int top_k, int tok_budget, long long n_sel, bool compact,

@@ -103,6 +103,17 @@ hipError_t launch_gather_selected(const void* k_cache, const void* v_cache, cons
                                   const int32_t* tok_slot, void* k_sel, void* v_sel, int B, int N, int C, int Hkv,
                                   int K, int Bt, int row_bytes, hipStream_t s);
 hipError_t launch_mfma_rate(int n_workgroups, int iters, float* sink, hipStream_t s);
+
+// Full-mask cache construction: joint rows [kept rows ; query rows] per sequence.
+struct JointArgs {
+  const void *q_pre, *k_cache, *v_cache, *q_qm, *k_qm, *v_qm;
+  const int32_t *chunk_idx, *tok_slot;
+  void *q_joint, *k_joint, *v_joint;
+  void *k_pref, *v_pref;   // optional [B][Hkv][Lj][d] copies of K, V (NULL: skipped)
+  int B, N, C, Lq, Lm, Hq, Hkv, G, D, K, Bt, Lj, qm_per_chunk, elem_bytes;
+  double rope_base;   // 0: no rotation
+};
+hipError_t launch_gather_joint(const JointArgs& a, hipStream_t s);
 hipError_t launch_token_rank(const float* tok_score, int32_t* tok_rank, int B, int N, int C, hipStream_t s);
 hipError_t launch_chunk_score(const float* qm_mass, float* chunk_score, int B, int N, int Hq, int Lq, int Lm,
                               hipStream_t s);

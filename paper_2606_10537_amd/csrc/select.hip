@@ -339,6 +339,116 @@ hipError_t launch_gather_selected(const void* k_cache, const void* v_cache, cons
   return hipGetLastError();
 }
 
+// Full-mask cache construction: the joint rows [kept rows ; L_q query rows] of
+// every sequence in the decode layout [B][Lj][H][d], Q and K moved to the
+// joint positions by the rotate-half rotary rotation, V copied.  Kept chunk k
+// (ascending) moves by k*(C+1), the query rows by (K-1)*(C+1); element i < d/2
+// pairs with i + d/2 at frequency base^(-2i/d).  The rotation runs in double
+// and is rounded once to the element type.  K and V also go, when asked, to
+// the compact prefix layout [B][Hkv][Lj][d] that the decoding steps read.
+// One workgroup per joint row: its d/2 cosines and sines (one shift) are
+// computed once into LDS, then the threads stream (tensor and head, pair of
+// 16-byte chunks c and c + d/2 elements) tasks through them.
+template <bool BF16>
+__global__ __launch_bounds__(256) void gather_joint_kernel(JointArgs a) {
+  constexpr int EPC = BF16 ? 8 : 4;   // elements per 16-byte chunk
+  __shared__ double cs_tab[64], sn_tab[64];
+  const size_t jrow = blockIdx.x;     // b * Lj + j
+  const int j = (int)(jrow % a.Lj), b = (int)(jrow / a.Lj);
+  const int C1 = a.C + 1, n_sel = a.K * (1 + a.Bt);
+  const bool kept = j < n_sel;
+  int kk = a.K - 1, slot = 0;
+  size_t n = 0, qm_row = 0;
+  if (kept) {
+    kk = j / (1 + a.Bt);
+    const int sl = j - kk * (1 + a.Bt);
+    slot = sl == 0 ? 0 : a.tok_slot[((size_t)b * a.K + kk) * a.Bt + sl - 1];
+    n = (size_t)b * a.N + a.chunk_idx[(size_t)b * a.K + kk];
+  } else {
+    qm_row = (a.qm_per_chunk ? (size_t)b * a.N : (size_t)b) * (size_t)(a.Lq + a.Lm) + (j - n_sel);
+  }
+  const bool rot = a.rope_base > 0.0;
+  if (rot) {
+    const double delta = (double)kk * C1;
+    for (int i = threadIdx.x; i < a.D / 2; i += 256) {
+      double sn, cs;
+      sincos(delta * pow(a.rope_base, -2.0 * i / a.D), &sn, &cs);
+      cs_tab[i] = cs;
+      sn_tab[i] = sn;
+    }
+    __syncthreads();
+  }
+  const int CP = a.D / EPC / 2;       // chunk pairs per row
+  const int tasks = (a.Hq + 2 * a.Hkv) * CP;
+  for (int task = threadIdx.x; task < tasks; task += 256) {
+    const int cp = task % CP, th = task / CP;
+    const int tensor = th < a.Hq ? 0 : (th < a.Hq + a.Hkv ? 1 : 2);   // Q, K, V
+    const int head = tensor == 0 ? th : (tensor == 1 ? th - a.Hq : th - a.Hq - a.Hkv);
+    const int H = tensor == 0 ? a.Hq : a.Hkv;
+    size_t src_el;
+    const void* src;
+    if (kept) {
+      if (tensor == 0) {
+        src = a.q_pre;
+        src_el = ((n * C1 + slot) * a.Hq + head) * a.D;
+      } else {
+        src = tensor == 1 ? a.k_cache : a.v_cache;
+        src_el = ((n * a.Hkv + head) * C1 + slot) * a.D;
+      }
+    } else {
+      src = tensor == 0 ? a.q_qm : (tensor == 1 ? a.k_qm : a.v_qm);
+      src_el = (qm_row * H + head) * a.D;
+    }
+    void* dst = tensor == 0 ? a.q_joint : (tensor == 1 ? a.k_joint : a.v_joint);
+    const size_t dst_el = (jrow * H + head) * a.D;
+    const u32x4* s4 = reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(src) + src_el * a.elem_bytes);
+    u32x4* d4 = reinterpret_cast<u32x4*>(reinterpret_cast<char*>(dst) + dst_el * a.elem_bytes);
+    u32x4 lo = s4[cp], hi = s4[cp + CP];
+    if (tensor < 2 && rot) {
+      float x[2][EPC];
+      Vec16<BF16>::load(s4 + cp, 0, x[0]);
+      Vec16<BF16>::load(s4 + cp + CP, 0, x[1]);
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) {
+        const int i = cp * EPC + e;   // pair index, 0 .. d/2 - 1
+        const double cs = cs_tab[i], sn = sn_tab[i];
+        const double p0 = x[0][e], p1 = x[1][e];
+        x[0][e] = (float)(p0 * cs - p1 * sn);
+        x[1][e] = (float)(p1 * cs + p0 * sn);
+      }
+      if constexpr (BF16) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          lo[q] = pack_bf16x2(x[0][2 * q], x[0][2 * q + 1]);
+          hi[q] = pack_bf16x2(x[1][2 * q], x[1][2 * q + 1]);
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          lo[q] = __float_as_uint(x[0][q]);
+          hi[q] = __float_as_uint(x[1][q]);
+        }
+      }
+    }
+    d4[cp] = lo;
+    d4[cp + CP] = hi;
+    void* pref = tensor == 1 ? a.k_pref : (tensor == 2 ? a.v_pref : nullptr);
+    if (pref) {
+      const size_t p_el = (((size_t)b * a.Hkv + head) * a.Lj + j) * a.D;
+      u32x4* p4 = reinterpret_cast<u32x4*>(reinterpret_cast<char*>(pref) + p_el * a.elem_bytes);
+      p4[cp] = lo;
+      p4[cp + CP] = hi;
+    }
+  }
+}
+
+hipError_t launch_gather_joint(const JointArgs& a, hipStream_t s) {
+  const dim3 grid((unsigned)((size_t)a.B * a.Lj));
+  if (a.elem_bytes == 2) hipLaunchKernelGGL(gather_joint_kernel<true>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(gather_joint_kernel<false>, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_key_mean(const void* k_cache, float* key_mean, int B, int N, int C, int Hkv, int head_dim,
                            bool bf16, hipStream_t s) {
   if (bf16)

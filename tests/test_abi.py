@@ -162,6 +162,31 @@ def test_select_ranked_validation(lib):
     assert call(dd=ctypes.byref(dims(tok_score_dir=-1).c())) == 2
 
 
+def test_gather_joint_validation(lib):
+    c = ctypes.byref(dims().c())
+
+    def call(k=2, bt=64, base=10000.0, ci=A, q=A, kq=A, qj=A, kp=None, vp=None, dd=c):
+        return lib.pd_gather_joint(dd, k, bt, ci, A, q, A, A, A, kq, A, base, qj, A, A, kp, vp, None)
+
+    assert call(dd=None) == 1
+    assert call(k=0) == 2
+    assert call(k=5) == 2            # top_k > N
+    assert call(bt=0) == 2
+    assert call(bt=129) == 2         # tok_budget > C
+    assert call(base=-1.0) == 2
+    assert call(base=float("nan")) == 2
+    assert call(base=float("inf")) == 2
+    assert call(ci=None) == 1
+    assert call(q=None) == 1
+    assert call(kq=None) == 1
+    assert call(qj=None) == 1
+    assert call(qj=MIS) == 4
+    assert call(kp=A) == 1           # one of k_pref / v_pref
+    assert call(vp=A) == 1
+    assert call(kp=A, vp=MIS) == 4
+    assert call(dd=ctypes.byref(dims(head_dim=96).c())) == 3
+
+
 def test_mfma_probe_validation(lib):
     assert lib.pd_mfma_rate_probe(0, 10, A, None) == 2
     assert lib.pd_mfma_rate_probe(4, 0, A, None) == 2

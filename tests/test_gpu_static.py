@@ -21,7 +21,7 @@ from gpu_path import (check_topk_rule_a, h64, random_decode_inputs, random_prefi
                       run_prefill, workspace)
 from paper_2606_10537_amd import _lib, synth
 from paper_2606_10537_amd._lib import PD_BF16, PD_FP32, Dims
-from test_gpu_parity import assert_out_close, bits
+from test_gpu_parity import assert_lse_close, assert_out_close, bits
 
 pytestmark = pytest.mark.gpu
 
@@ -131,5 +131,6 @@ def test_compact_decode_parity(case):
         for h in range(Hq):
             ro, rl = oracle.decode_compact_unit_ref(qd, kd, vd, ksh, vsh, h64(kst), h64(vst), n_static, b, h)
             assert_out_close(d, h64(o[b, :, h]), ro, f"compact decode O (b={b}, h={h})")
-            atol = 2e-3 if d.dtype == PD_BF16 else 1e-4
-            np.testing.assert_allclose(h64(lse[b, h]), rl, rtol=1e-5, atol=atol)
+            g = h // (Hq // Hkv)
+            keys = np.concatenate([ksh[b, g], h64(kst)[b, :n_static, g], kd[b, :, g]])
+            assert_lse_close(d, h64(lse[b, h]), rl, qd[b, :, h], keys, f"compact decode LSE (b={b}, h={h})")
