@@ -131,54 +131,107 @@ constexpr int kScoreRows = 128;
 int select_row_splits(int Ld) { return (Ld + kScoreRows - 1) / kScoreRows; }
 
 // Chunk-score terms of one (b, h, row split): scale * <(1/L_d) sum_r q_r, kbar[b][n][h/G]> for all n.
-// The dot products run 8 lanes per chunk (D/8 dimensions each, all loads in
-// flight at once), reduced by a fixed xor butterfly.
+// Latency-bound (a few KB per workgroup), so every load of a thread is issued
+// before the first use: the key means of the first 32 chunks, then the thread's
+// share of the rows (fully unrolled).  The row sums are reduced through LDS in
+// a fixed order; the dot products run 8 lanes per chunk (D/8 dimensions each),
+// reduced by a fixed xor butterfly.
 template <bool BF16, int D>
 __global__ __launch_bounds__(256) void qscore_kernel(const void* q_dec, const float* key_mean, float* partial,
                                                       int N, int Hq, int Hkv, int G, int rows, int row0, int bstride,
                                                       int NS, float scale) {
   constexpr int SL = D / 8;
-  __shared__ float red[2048];
+  constexpr int E = Vec16<BF16>::E;
+  constexpr int TPR = D / E, NG = 256 / TPR, IT = kScoreRows / NG;
+  __shared__ float red[NG * D];
   __shared__ float qp[D];
-  const int sp = blockIdx.x % NS;
-  const int bh = blockIdx.x / NS;
-  const int h = bh % Hq, b = bh / Hq;
-  const int r0 = sp * kScoreRows, r1 = min(rows, r0 + kScoreRows);
-  rows_mean<BF16>(q_dec, (((size_t)b * bstride + row0 + r0) * Hq + h) * D, (size_t)Hq * D, r1 - r0, D, 1.0f / rows,
-                  qp, red);
-  __syncthreads();
+  // Heads fastest: workgroups that run together read whole contiguous rows.
+  const int h = blockIdx.x % Hq;
+  const int sp = (blockIdx.x / Hq) % NS;
+  const int b = blockIdx.x / (Hq * NS);
+  const int t = threadIdx.x;
+  const int r0 = sp * kScoreRows, nr = min(rows, r0 + kScoreRows) - r0;
   const float* kb = key_mean + ((size_t)b * N * Hkv + h / G) * D;
-  const int j = threadIdx.x & 7;
+  const int j = t & 7;
+  f32x4 kv[SL / 4];
+  {
+    const int n = t >> 3;
+    if (n < N) {
+      const f32x4* kr = reinterpret_cast<const f32x4*>(kb + (size_t)n * Hkv * D + j * SL);
+#pragma unroll
+      for (int i = 0; i < SL / 4; ++i) kv[i] = kr[i];
+    }
+  }
+  const int c = t % TPR, rg = t / TPR;
+  const size_t base = (((size_t)b * bstride + row0 + r0) * Hq + h) * D + c * E;
+  u32x4 w[IT];
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const int r = rg + it * NG;
+    w[it] = r < nr ? *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(q_dec) +
+                                                      (base + (size_t)r * Hq * D) * (BF16 ? 2 : 4))
+                   : u32x4{0u, 0u, 0u, 0u};
+  }
+  float acc[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] = 0.f;
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    if constexpr (BF16) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        acc[2 * i] += __uint_as_float(w[it][i] << 16);
+        acc[2 * i + 1] += __uint_as_float(w[it][i] & 0xffff0000u);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[i] += __uint_as_float(w[it][i]);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < E; ++e) red[rg * D + c * E + e] = acc[e];
+  __syncthreads();
+  if (t < D) {
+    float sum = 0.f;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) sum += red[g * D + t];
+    qp[t] = sum * (1.0f / rows);
+  }
+  __syncthreads();
   float q[SL];
 #pragma unroll
   for (int i = 0; i < SL; ++i) q[i] = qp[j * SL + i];
   for (int n0 = 0; n0 < N; n0 += 32) {
-    const int n = n0 + (threadIdx.x >> 3);
-    float acc = 0.f;
-    if (n < N) {
+    const int n = n0 + (t >> 3);
+    if (n0 > 0 && n < N) {
       const f32x4* kr = reinterpret_cast<const f32x4*>(kb + (size_t)n * Hkv * D + j * SL);
-      f32x4 v[SL / 4];
 #pragma unroll
-      for (int i = 0; i < SL / 4; ++i) v[i] = kr[i];
+      for (int i = 0; i < SL / 4; ++i) kv[i] = kr[i];
+    }
+    float acc2 = 0.f;
+    if (n < N) {
 #pragma unroll
       for (int i = 0; i < SL / 4; ++i)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc = fmaf(q[4 * i + e], v[i][e], acc);
+        for (int e = 0; e < 4; ++e) acc2 = fmaf(q[4 * i + e], kv[i][e], acc2);
     }
-    acc += __shfl_xor(acc, 1);
-    acc += __shfl_xor(acc, 2);
-    acc += __shfl_xor(acc, 4);
-    if (j == 0 && n < N) partial[((size_t)b * N + n) * Hq * NS + (size_t)h * NS + sp] = acc * scale;
+    acc2 += __shfl_xor(acc2, 1);
+    acc2 += __shfl_xor(acc2, 2);
+    acc2 += __shfl_xor(acc2, 4);
+    if (j == 0 && n < N) partial[((size_t)b * N + n) * Hq * NS + (size_t)h * NS + sp] = acc2 * scale;
   }
 }
 
-// neg = 1 keeps the K lowest scores instead of the K highest.
+// neg = 1 keeps the K lowest scores instead of the K highest.  One workgroup
+// per (sequence, kept chunk k): all compute the chunk ranking, workgroup k then
+// lists the kept tokens of the k-th kept chunk.
 __global__ __launch_bounds__(256) void select_kernel(const float* partial, const int32_t* tok_rank,
                                                       float* chunk_score, int32_t* chunk_idx, int32_t* tok_slot,
                                                       int N, int C, int K, int Bt, int T, int Npad, int neg) {
   extern __shared__ __attribute__((aligned(16))) uint64_t keys[];
   __shared__ int my_chunk;
-  __shared__ int scan[2][256];
+  __shared__ int rankv[256];
+  __shared__ int wsum[4];
   const int b = blockIdx.x / K, k = blockIdx.x % K;
   const int t = threadIdx.x;
 
@@ -206,34 +259,54 @@ __global__ __launch_bounds__(256) void select_kernel(const float* partial, const
     }
   }
   __syncthreads();
-  bitonic_sort(keys, Npad);
-  // The K kept chunks (first K keys) in ascending index order.
-  for (int i = t; i < K; i += 256) {
-    const int x = (int)(uint32_t)keys[i];
-    int pos = 0;
-    for (int j = 0; j < K; ++j) pos += (int)(uint32_t)keys[j] < x;
-    if (pos == k) my_chunk = x;
-    if (k == 0) chunk_idx[(size_t)b * K + pos] = x;
+  // The K kept chunks (the K smallest keys) in ascending index order.  Up to
+  // 256 chunks: each chunk's rank by counting the smaller keys (keys are
+  // distinct: the index is in the low bits); beyond, a bitonic sort.
+  if (N <= 256) {
+    if (t < N) {
+      const uint64_t me = keys[t];
+      int r = 0;
+      for (int i = 0; i < N; ++i) r += keys[i] < me;
+      rankv[t] = r;
+    }
+    __syncthreads();
+    if (t < N && rankv[t] < K) {
+      int pos = 0;
+      for (int i = 0; i < t; ++i) pos += rankv[i] < K;
+      if (pos == k) my_chunk = t;
+      if (k == 0) chunk_idx[(size_t)b * K + pos] = t;
+    }
+  } else {
+    bitonic_sort(keys, Npad);
+    for (int i = t; i < K; i += 256) {
+      const int x = (int)(uint32_t)keys[i];
+      int pos = 0;
+      for (int j = 0; j < K; ++j) pos += (int)(uint32_t)keys[j] < x;
+      if (pos == k) my_chunk = x;
+      if (k == 0) chunk_idx[(size_t)b * K + pos] = x;
+    }
   }
   __syncthreads();
   const int32_t* rk = tok_rank + ((size_t)b * N + my_chunk) * C;
 
   // Kept tokens (rank < Bt) in ascending order: counts over contiguous segments,
-  // an exclusive block scan, then each segment writes its slots.
+  // an exclusive scan (within each wave by shuffles, then across the 4 waves),
+  // then each segment writes its slots.
   const int seg = (C + 255) / 256;
   const int j0 = t * seg, j1 = min(C, j0 + seg);
   int cnt = 0;
   for (int j = j0; j < j1; ++j) cnt += rk[j] < Bt;
-  scan[0][t] = cnt;
-  __syncthreads();
-  int cur = 0;
-  for (int w = 1; w < 256; w <<= 1) {
-    const int v = scan[cur][t] + (t >= w ? scan[cur][t - w] : 0);
-    scan[cur ^ 1][t] = v;
-    cur ^= 1;
-    __syncthreads();
+  const int lane = t & 63, wv = t >> 6;
+  int inc = cnt;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(inc, o);
+    if (lane >= o) inc += y;
   }
-  int pos = scan[cur][t] - cnt;
+  if (lane == 63) wsum[wv] = inc;
+  __syncthreads();
+  int pos = inc - cnt;
+  for (int w = 0; w < wv; ++w) pos += wsum[w];
   int32_t* out = tok_slot + ((size_t)b * K + k) * Bt;
   for (int j = j0; j < j1; ++j)
     if (rk[j] < Bt) out[pos++] = j + 1;
