@@ -338,6 +338,19 @@ __device__ __forceinline__ void wave_step(WaveState<D> (&st)[NH], uint32_t (&pk)
   if (!deferred || last) pv_phase<D, NH>(st, pk, Vs, fa);
 }
 
+// Completes the loads of the Q fragments here, before the sweep.  The compiler
+// does not see the tile DMAs (inline assembly): a Q load it still counted as
+// pending would make it wait for every load in flight (s_waitcnt vmcnt(0)),
+// tile DMAs included, at the fragment's first use in every tile.  Consuming
+// the registers in an empty asm statement puts that one wait here instead.
+template <int D, int NH>
+__device__ __forceinline__ void q_landed(const WaveState<D> (&st)[NH]) {
+#pragma unroll
+  for (int j = 0; j < NH; ++j)
+#pragma unroll
+    for (int ks = 0; ks < Tile<D>::KS; ++ks) asm volatile("" ::"v"(st[j].qf[ks]));
+}
+
 template <int D>
 __device__ __forceinline__ void wave_init(WaveState<D>& st) {
 #pragma unroll
@@ -387,20 +400,31 @@ struct RowPtr {
 // tile row r (already clamped to a valid row).  All row pointers are formed
 // before the first DMA is issued: an LDS read (a row table) after a DMA would
 // make the compiler wait for it.
-template <int D, class Row>
-__device__ __forceinline__ void dma_tile(uint16_t* Kd, uint16_t* Vd, int wave, int lane, Row&& row) {
+template <int D>
+__device__ __forceinline__ int dma_row(int wave, int lane, int j) {
+  return ((wave * Tile<D>::BPW + j) & 3) * 16 + (lane >> 2);
+}
+
+template <int D>
+__device__ __forceinline__ void dma_tile_rows(uint16_t* Kd, uint16_t* Vd, int wave, int lane,
+                                              const RowPtr (&rp)[Tile<D>::BPW]) {
   using T = Tile<D>;
-  RowPtr rp[T::BPW];
-#pragma unroll
-  for (int j = 0; j < T::BPW; ++j) rp[j] = row(((wave * T::BPW + j) & 3) * 16 + (lane >> 2));
 #pragma unroll
   for (int j = 0; j < T::BPW; ++j) {
     const int blk = wave * T::BPW + j;
-    const int r = (blk & 3) * 16 + (lane >> 2);
+    const int r = dma_row<D>(wave, lane, j);
     const int c = 4 * (blk >> 2) + ((lane & 3) ^ ((r >> 2) & 3));
     dma16(rp[j].k + 8 * c, Kd + blk * 512);
     dma16(rp[j].v + 8 * c, Vd + blk * 512);
   }
+}
+
+template <int D, class Row>
+__device__ __forceinline__ void dma_tile(uint16_t* Kd, uint16_t* Vd, int wave, int lane, Row&& row) {
+  RowPtr rp[Tile<D>::BPW];
+#pragma unroll
+  for (int j = 0; j < Tile<D>::BPW; ++j) rp[j] = row(dma_row<D>(wave, lane, j));
+  dma_tile_rows<D>(Kd, Vd, wave, lane, rp);
 }
 
 // Wait until this wave has at most `newer` tiles of DMA in flight: tile DMAs
@@ -495,6 +519,7 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void prefill_bf16_kernel(PrefillArg
       st[j].qf[ks] = src ? __builtin_bit_cast(bf16x8, ld16(src + 16 * ks + 8 * grp)) : bf16x8{0};
     wave_init(st[j]);
   }
+  q_landed<D, T::NH>(st);
   const FragAddr fa(lane);
 
   // Row r of the chunk sequence lives at base + r*HD (HD = H_kv*d elements), with
@@ -614,6 +639,7 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void decode_bf16_kernel(DecodeArgs 
       st[j].qf[ks] = src ? __builtin_bit_cast(bf16x8, ld16(src + 16 * ks + 8 * grp)) : bf16x8{0};
     wave_init(st[j]);
   }
+  q_landed<D, T::NH>(st);
   const FragAddr fa(lane);
 
   // This shard's tiles.
@@ -655,15 +681,44 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void decode_bf16_kernel(DecodeArgs 
   const int tab_hi = max(j_hi - j_lo - 1, 0);
   const int n_static = p.n_static;
   int* const rowtab_p = rowtab;
-  auto dma = [=](int t, uint16_t* Kd, uint16_t* Vd) {
+  // A whole gathered tile takes this lane's row codes from the row table.
+  // They are read one tile ahead (right after the previous tile's DMA) and
+  // kept raw until used, so that issuing a DMA after the barrier needs no LDS
+  // read and no wait.
+  auto read_tab = [=](int t, unsigned (&o)[T::BPW]) {
+    const int* tab = rowtab_p + (t * T::BN - j_lo);
+#pragma unroll
+    for (int j = 0; j < T::BPW; ++j) o[j] = (unsigned)tab[dma_row<D>(wave, lane, j)];
+  };
+  unsigned nxt[T::BPW];
+  int nxt_t = -1;
+  auto dma = [&](int t, uint16_t* Kd, uint16_t* Vd) {
     const int* rowtab = rowtab_p;
     const int r0 = t * T::BN;
     if (r0 + T::BN <= n_sel) {
       // Whole tile gathered from the cache.
-      const int* tab = rowtab + (r0 - j_lo);
+      unsigned o[T::BPW];
+      if (nxt_t == t) {
+#pragma unroll
+        for (int j = 0; j < T::BPW; ++j) o[j] = nxt[j];
+      } else {
+        read_tab(t, o);
+      }
+      RowPtr rp[T::BPW];
+#pragma unroll
+      for (int j = 0; j < T::BPW; ++j) rp[j] = RowPtr{kc + o[j] * D, vc + o[j] * D};
+      dma_tile_rows<D>(Kd, Vd, wave, lane, rp);
+      if (r0 + 2 * T::BN <= n_sel && t + 1 < t_end) {
+        read_tab(t + 1, nxt);
+        nxt_t = t + 1;
+      }
+    } else if (r0 >= n_sel) {
+      // No gathered row: static rows, then own rows.
       dma_tile<D>(Kd, Vd, wave, lane, [=](int r) {
-        const unsigned off = (unsigned)tab[r] * D;
-        return RowPtr{kc + off, vc + off};
+        const int j = min(r0 + r, L_kv - 1);
+        const unsigned off = (unsigned)(j * HD);
+        const bool stat = j < n_sel + n_static;
+        return RowPtr{(stat ? ks_ : kd_) + off, (stat ? vs_ : vd_) + off};
       });
     } else {
       dma_tile<D>(Kd, Vd, wave, lane, [=](int r) {
