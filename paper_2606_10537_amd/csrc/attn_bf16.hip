@@ -769,81 +769,80 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void decode_bf16_kernel(DecodeArgs 
 }
 
 // ---------------------------------------------------------------------------
-// Eq. 5, first sum: for each content token j, the softmax mass the L_q query
-// rows put on it, summed over heads, plus (unless only the query-to-chunk
-// direction is asked for) the second sum (per-head query-column mass of row j,
-// written by the prefill kernel).  Workgroup = (b, n, 64 content
-// columns); wave w handles heads w, w+4, ...  S = Q_q K_c^T on MFMA, then
-// exp2(S*scale - lse2(row)) with the query rows' final LSE from the prefill.
+// Eq. 5, first sum, one workgroup per (b, n, h): the query rows of head h and
+// their final LSE are staged in LDS (up to 128 rows per pass), and the 4 waves
+// split the C content keys in 32-key blocks, so every key row is read from HBM
+// once.  S = Q_q K_c^T on MFMA (A: query rows from LDS, B: key rows from
+// global memory, the next block's prefetched), each key's mass exp2(S*scale -
+// lse2(row)) summed in the lane that holds the key.  The head's sum is added
+// in place to its per-head second sum (written by the prefill), or replaces
+// it for the query-to-chunk score; head_sum_rank_kernel then sums the heads.
+// Query row r's 16-byte chunk c sits at chunk c ^ (r % CH) of its LDS row, so
+// that the 16 lanes of a ds_read_b128 pass (16 rows, one chunk) hit 16
+// different bank groups.
 template <int D>
-__global__ __launch_bounds__(256) void escore_bf16_kernel(EscoreArgs p) {
-  constexpr int KS = D / 16;
-  __shared__ float red[4][64];
+__global__ __launch_bounds__(256) void escore2_bf16_kernel(EscoreArgs p) {
+  constexpr int KS = D / 16, CH = D / 8, QB = 128;
+  __shared__ __attribute__((aligned(16))) uint16_t qs[QB * D];
+  __shared__ __attribute__((aligned(16))) float ls[QB];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, grp = lane >> 5;
-  int lid = blockIdx.x;
-  const int cb = lid % p.n_cb;
-  lid /= p.n_cb;
-  const int n = lid % p.N;
-  const int b = lid / p.N;
-  const int C1 = p.C + 1;
-  const size_t chunk = (size_t)b * p.N + n;
-  const size_t qm_base = (p.qm_per_chunk ? chunk : (size_t)b) * (size_t)(p.Lq + p.Lm);
-  const int n_qb = (p.Lq + 31) / 32;
-
-  float colsum[2] = {0.f, 0.f};
-  for (int h = wave; h < p.Hq; h += 4) {
-    const int g = h / p.G;
-    bf16x8 kf[2][KS];
+  const size_t bnh = blockIdx.x;   // (b * N + n) * Hq + h
+  const int h = (int)(bnh % p.Hq);
+  const size_t bn = bnh / p.Hq;
+  const int b = (int)(bn / p.N);
+  const int g = h / p.G, C1 = p.C + 1;
+  const size_t qm_base = (p.qm_per_chunk ? bn : (size_t)b) * (size_t)(p.Lq + p.Lm);
+  const uint16_t* kbase = p.k_cache + ((bn * p.Hkv + g) * C1 + 1) * D;   // content row j at kbase + j*D
+  const float* lse = p.lse_q + bnh * p.Lq;
+  float* ph = p.part_io + bnh * p.C;
+  const int nkb = (p.C + 31) / 32;
+  auto load_k = [&](int kb, bf16x8 (&kf)[KS]) {
+    const int j = kb * 32 + l32;
+    const uint16_t* src = j < p.C ? kbase + (size_t)j * D : nullptr;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const int j = cb * 64 + 32 * kb + l32;
-      const uint16_t* src = j < p.C ? p.k_cache + ((chunk * p.Hkv + g) * C1 + 1 + j) * D : nullptr;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        kf[kb][ks] = src ? __builtin_bit_cast(bf16x8, ld16(src + 16 * ks + 8 * grp)) : bf16x8{0};
+    for (int ks = 0; ks < KS; ++ks) kf[ks] = src ? __builtin_bit_cast(bf16x8, ld16(src + 16 * ks + 8 * grp)) : bf16x8{0};
+  };
+  for (int r0 = 0; r0 < p.Lq; r0 += QB) {
+    const int nr = min(QB, p.Lq - r0);
+    if (r0 > 0) __syncthreads();   // the previous pass is done with qs, ls
+    for (int u = tid; u < QB * CH; u += 256) {
+      const int r = u / CH, c = u % CH;
+      const u32x4 v = r < nr ? ld16(p.q_qm + ((qm_base + r0 + r) * p.Hq + h) * D + 8 * c) : u32x4{0u, 0u, 0u, 0u};
+      st16(qs + r * D + 8 * (c ^ (r % CH)), v);
     }
-    const float* lse = p.lse_q + (chunk * p.Hq + h) * p.Lq;
-    for (int qb = 0; qb < n_qb; ++qb) {
-      const int qrow = qb * 32 + l32;
-      const uint16_t* qsrc = qrow < p.Lq ? p.q_qm + ((qm_base + qrow) * p.Hq + h) * D : nullptr;
-      bf16x8 qa[KS];
+    for (int r = tid; r < QB; r += 256) ls[r] = r < nr ? lse[r0 + r] : INFINITY;
+    __syncthreads();
+    bf16x8 kf[KS], kn[KS];
+    if (wave < nkb) load_k(wave, kf);
+    for (int kb = wave; kb < nkb; kb += 4) {
+      if (kb + 4 < nkb) load_k(kb + 4, kn);
+      float colsum = 0.f;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        qa[ks] = qsrc ? __builtin_bit_cast(bf16x8, ld16(qsrc + 16 * ks + 8 * grp)) : bf16x8{0};
-      // Row (query) of element r: qb*32 + 8*(r/4) + 4*grp + r%4.
-      float lrow[16];
+      for (int qb = 0; qb < QB / 32; ++qb) {
+        if (qb * 32 >= nr) break;
+        const int row = qb * 32 + l32;
+        f32x16 sacc = f32x16{0};
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int q = qb * 32 + 8 * (r >> 2) + 4 * grp + (r & 3);
-        lrow[r] = q < p.Lq ? lse[q] : INFINITY;
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8 qa = __builtin_bit_cast(bf16x8, ld16(qs + row * D + 8 * ((2 * ks + grp) ^ (row % CH))));
+          sacc = mfma32x32x16(qa, kf[ks], sacc);
+        }
+        // Row (query) of element r: qb*32 + 8*(r/4) + 4*grp + r%4.
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const f32x4 l4 = *reinterpret_cast<const f32x4*>(ls + qb * 32 + 8 * i + 4 * grp);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) colsum += fast_exp2(sacc[4 * i + e] * p.scale_log2 - l4[e]);
+        }
       }
+      const float v = colsum + __shfl_xor(colsum, 32);
+      const int j = kb * 32 + l32;
+      if (grp == 0 && j < p.C) ph[j] = (p.q2c && r0 == 0) ? v : ph[j] + v;
+      if (kb + 4 < nkb) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        f32x16 s = f32x16{0};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) s = mfma32x32x16(qa[ks], kf[kb][ks], s);
-        float acc = 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc += fast_exp2(s[r] * p.scale_log2 - lrow[r]);
-        colsum[kb] += acc;
+        for (int ks = 0; ks < KS; ++ks) kf[ks] = kn[ks];
       }
-    }
-  }
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb) {
-    const float v = colsum[kb] + __shfl_xor(colsum[kb], 32);
-    if (grp == 0) red[wave][32 * kb + l32] = v;
-  }
-  __syncthreads();
-  if (tid < 64) {
-    const int j = cb * 64 + tid;
-    if (j < p.C) {
-      float e = 0.f;
-      if (!p.q2c)
-        for (int h = 0; h < p.Hq; ++h) e += p.part_i[(chunk * p.Hq + h) * p.C + j];
-      e += ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
-      p.tok_score[chunk * p.C + j] = e;
     }
   }
 }
@@ -870,7 +869,7 @@ hipError_t launch_decode_bf16(const DecodeArgs& a, int head_dim, hipStream_t s) 
 
 template <int D>
 static hipError_t launch_escore_d(const EscoreArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(escore_bf16_kernel<D>, dim3(a.total), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(escore2_bf16_kernel<D>, dim3(a.B * a.N * a.Hq), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 hipError_t launch_escore_bf16(const EscoreArgs& a, int head_dim, hipStream_t s) {

@@ -287,6 +287,7 @@ pd_status pd_prefill_chunks(const pd_dims* d, const void* q_pre, const void* k_p
   e.q_qm = a.q_qm;
   e.k_cache = a.k_cache;
   e.part_i = a.part_i;
+  e.part_io = a.part_i;
   e.lse_q = a.lse_q;
   e.tok_score = tok_score;
   e.B = a.B;
@@ -309,6 +310,8 @@ pd_status pd_prefill_chunks(const pd_dims* d, const void* q_pre, const void* k_p
     if (err != hipSuccess) return hip_status(err, "prefill kernel");
     err = pd::launch_escore_bf16(e, d->head_dim, s);
     if (err != hipSuccess) return hip_status(err, "token-score kernel");
+    err = pd::launch_head_sum_rank(a.part_i, tok_score, tok_rank, a.B, a.N, a.Hq, a.C, s);
+    if (err != hipSuccess) return hip_status(err, "token-rank kernel");
   } else {
     err = pd::launch_prefill_f32(a, d->head_dim, s);
     if (err != hipSuccess) return hip_status(err, "prefill kernel");
@@ -316,9 +319,9 @@ pd_status pd_prefill_chunks(const pd_dims* d, const void* q_pre, const void* k_p
     if (err != hipSuccess) return hip_status(err, "cache copy kernel");
     err = pd::launch_escore_f32(e, d->head_dim, s);
     if (err != hipSuccess) return hip_status(err, "token-score kernel");
+    err = pd::launch_token_rank(tok_score, tok_rank, a.B, a.N, a.C, s);
+    if (err != hipSuccess) return hip_status(err, "token-rank kernel");
   }
-  err = pd::launch_token_rank(tok_score, tok_rank, a.B, a.N, a.C, s);
-  if (err != hipSuccess) return hip_status(err, "token-rank kernel");
   if (chunk_score) {
     err = pd::launch_chunk_score(a.qm_mass, chunk_score, a.B, a.N, a.Hq, a.Lq, a.Lm, s);
     if (err != hipSuccess) return hip_status(err, "chunk-score kernel");

@@ -46,6 +46,7 @@ struct PrefillArgs {
 struct EscoreArgs {
   const uint16_t *q_qm, *k_cache;
   const float *part_i, *lse_q;
+  float* part_io;    // bf16 path: per-head sums [B][N][Hq][C], updated in place (same buffer as part_i)
   float* tok_score;
   int B, N, C, Lq, Lm, Hq, Hkv, G, n_cb, total, qm_per_chunk;
   int q2c;           // 1: only the query rows' mass on the token (query-to-chunk score)
@@ -115,6 +116,9 @@ struct JointArgs {
 };
 hipError_t launch_gather_joint(const JointArgs& a, hipStream_t s);
 hipError_t launch_token_rank(const float* tok_score, int32_t* tok_rank, int B, int N, int C, hipStream_t s);
+// e = sum over the H_q heads of the per-head sums (fixed order), then the ranks.
+hipError_t launch_head_sum_rank(const float* per_head, float* tok_score, int32_t* tok_rank, int B, int N, int Hq,
+                                int C, hipStream_t s);
 hipError_t launch_chunk_score(const float* qm_mass, float* chunk_score, int B, int N, int Hq, int Lq, int Lm,
                               hipStream_t s);
 hipError_t launch_select_ranked(const float* chunk_score, int lowest, const int32_t* tok_rank, int32_t* chunk_idx,

@@ -120,6 +120,36 @@ __global__ __launch_bounds__(256) void token_rank_kernel(const float* tok_score,
   for (int i = threadIdx.x; i < C; i += 256) tok_rank[bn * C + (uint32_t)keys[i]] = i;
 }
 
+// e of one chunk = sum over the H_q heads of the per-head sums (heads in
+// ascending order), written out, then every token's rank as token_rank_kernel.
+__global__ __launch_bounds__(256) void head_sum_rank_kernel(const float* per_head, float* tok_score,
+                                                             int32_t* tok_rank, int Hq, int C, int Cpad) {
+  extern __shared__ __attribute__((aligned(16))) uint64_t keys[];
+  const size_t bn = blockIdx.x;
+  const float* ph = per_head + bn * Hq * C;
+  for (int j = threadIdx.x; j < Cpad; j += 256) {
+    if (j < C) {
+      float e = 0.f;
+      for (int h = 0; h < Hq; ++h) e += ph[(size_t)h * C + j];
+      tok_score[bn * C + j] = e;
+      keys[j] = rank_key(e, j);
+    } else {
+      keys[j] = ~0ull;
+    }
+  }
+  __syncthreads();
+  bitonic_sort(keys, Cpad);
+  for (int i = threadIdx.x; i < C; i += 256) tok_rank[bn * C + (uint32_t)keys[i]] = i;
+}
+
+hipError_t launch_head_sum_rank(const float* per_head, float* tok_score, int32_t* tok_rank, int B, int N, int Hq,
+                                int C, hipStream_t s) {
+  const int Cpad = next_pow2(C);
+  hipLaunchKernelGGL(head_sum_rank_kernel, dim3(B * N), dim3(256), (size_t)Cpad * 8, s, per_head, tok_score, tok_rank,
+                     Hq, C, Cpad);
+  return hipGetLastError();
+}
+
 hipError_t launch_token_rank(const float* tok_score, int32_t* tok_rank, int B, int N, int C, hipStream_t s) {
   const int Cpad = next_pow2(C);
   hipLaunchKernelGGL(token_rank_kernel, dim3(B * N), dim3(256), (size_t)Cpad * 8, s, tok_score, tok_rank, C, Cpad);
