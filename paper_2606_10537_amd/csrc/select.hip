@@ -130,6 +130,7 @@ __global__ __launch_bounds__(256) void head_sum_rank_kernel(const float* per_hea
   for (int j = threadIdx.x; j < Cpad; j += 256) {
     if (j < C) {
       float e = 0.f;
+#pragma unroll 16
       for (int h = 0; h < Hq; ++h) e += ph[(size_t)h * C + j];
       tok_score[bn * C + j] = e;
       keys[j] = rank_key(e, j);
