@@ -639,7 +639,6 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void decode_bf16_kernel(DecodeArgs 
       st[j].qf[ks] = src ? __builtin_bit_cast(bf16x8, ld16(src + 16 * ks + 8 * grp)) : bf16x8{0};
     wave_init(st[j]);
   }
-  q_landed<D, T::NH>(st);
   const FragAddr fa(lane);
 
   // This shard's tiles.
@@ -734,6 +733,8 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void decode_bf16_kernel(DecodeArgs 
       });
     }
   };
+  // The Q loads overlap the row-table loads above; both have landed here.
+  q_landed<D, T::NH>(st);
   auto no_hook = [](int, const uint16_t*, const uint16_t*) {};
   uint32_t pk_prev[T::NH][16];
   const bool deferred = wave_group(wave) != 0;
