@@ -487,6 +487,7 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void prefill_bf16_kernel(PrefillArg
   using T = Tile<D>;
   __shared__ __attribute__((aligned(1024))) uint16_t K0[T::TILE], K1[T::TILE], K2[T::TILE], K3[T::TILE];
   __shared__ __attribute__((aligned(1024))) uint16_t V0[T::TILE], V1[T::TILE], V2[T::TILE], V3[T::TILE];
+  __shared__ __attribute__((aligned(16))) float kacc[T::NT / T::CH * D];   // content-key sums, one slot per thread
   uint16_t* const Kb[4] = {K0, K1, K2, K3};   // the first T::S are used
   uint16_t* const Vb[4] = {V0, V1, V2, V3};
 
@@ -543,20 +544,37 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void prefill_bf16_kernel(PrefillArg
   // Each KV tile of the (b, n, kv head) group is written to the cache by exactly
   // one workgroup of that group (query tile t % n_qt of head g*G + (t / n_qt) % G),
   // from the landed LDS tile: thread tid copies logical chunks tid + NT i.
+  // Thread tid always handles 16-byte chunk tid % CH of the rows it copies, so
+  // its content-key sums live in its own LDS slot kacc[tid / CH][8 (tid % CH) ..]
+  // (no other thread touches it until the reduction after the sweep).
+  float* const kslot = kacc + (tid / T::CH) * D + 8 * (tid % T::CH);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) kslot[e] = 0.f;
   auto cache_write = [&](int t, const uint16_t* Ks, const uint16_t* Vs) {
     const bool writer = (t % p.n_qt == qt) && ((t / p.n_qt) % p.G == h % p.G);
     if (!writer) return;
     const size_t base = (chunk * p.Hkv + g) * C1;
+    float ksum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int i = 0; i < T::BN * T::CH / T::NT; ++i) {
       const int u = tid + T::NT * i;
       const int r = u / T::CH, c = u % T::CH;
       const int row = t * T::BN + r;
       if (row < C1) {
-        st16(p.k_cache + (base + row) * D + 8 * c, ld16(Ks + tile_off(r, c)));
+        const u32x4 kv = ld16(Ks + tile_off(r, c));
+        st16(p.k_cache + (base + row) * D + 8 * c, kv);
         st16(p.v_cache + (base + row) * D + 8 * c, ld16(Vs + tile_off(r, c)));
+        if (row >= 1) {   // content rows only (the BOS row is not part of the key mean)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            ksum[2 * q] += __uint_as_float(kv[q] << 16);
+            ksum[2 * q + 1] += __uint_as_float(kv[q] & 0xffff0000u);
+          }
+        }
       }
     }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) kslot[e] += ksum[e];
   };
 
   const int qc_lo = C1, qc_hi = C1 + p.Lq;   // query columns counted by Eq. 5
@@ -574,6 +592,14 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void prefill_bf16_kernel(PrefillArg
                 wave_step<D, T::NH, true>(st, pk_prev, deferred, t == 0, last, ks, vs, vs_prev, fa, grp,
                                           p.scale_log2, kv_valid, mr);
               });
+  // This workgroup's content-key sums: the thread slots summed in a fixed
+  // order, one vector per (b, n, kv head, writer slot qt*G + h%G).
+  __syncthreads();
+  if (tid < D) {
+    float sum = 0.f;
+    for (int r = 0; r < T::NT / T::CH; ++r) sum += kacc[r * D + tid];
+    p.km_part[((chunk * p.Hkv + g) * (size_t)(p.n_qt * p.G) + qt * p.G + h % p.G) * D + tid] = sum;
+  }
   if (!wave_active) return;
 
 #pragma unroll

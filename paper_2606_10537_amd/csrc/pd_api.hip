@@ -88,15 +88,23 @@ float scale_of(const pd_dims* d) { return d->sm_scale > 0.f ? d->sm_scale : 1.0f
 
 // --- workspace layouts -------------------------------------------------------
 struct PrefillWs {
-  size_t part_i, lse_q, qm_mass, total;
+  size_t part_i, lse_q, qm_mass, km_part, total;
 };
+// Writer slots of the key-mean partial sums: one per (query tile, head of the
+// KV group) of the bf16 prefill.
+int km_slots(const pd_dims* d) {
+  const long long sc = 1LL + d->chunk_len + d->q_len + d->m_len;
+  return cdiv(sc, pd::kBf16Rows) * (d->n_heads_q / d->n_heads_kv);
+}
 PrefillWs prefill_ws(const pd_dims* d) {
   PrefillWs w;
   const size_t bnh = (size_t)d->batch * d->n_chunks * d->n_heads_q;
+  const size_t bng = (size_t)d->batch * d->n_chunks * d->n_heads_kv;
   w.part_i = 0;
   w.lse_q = round_up(bnh * d->chunk_len * sizeof(float));
   w.qm_mass = w.lse_q + round_up(bnh * d->q_len * sizeof(float));
-  w.total = w.qm_mass + round_up(bnh * (d->q_len + d->m_len) * sizeof(float));
+  w.km_part = w.qm_mass + round_up(bnh * (d->q_len + d->m_len) * sizeof(float));
+  w.total = w.km_part + (d->dtype == PD_BF16 ? round_up(bng * km_slots(d) * d->head_dim * sizeof(float)) : 0);
   return w;
 }
 
@@ -267,6 +275,7 @@ pd_status pd_prefill_chunks(const pd_dims* d, const void* q_pre, const void* k_p
   a.part_i = (float*)(ws + w.part_i);
   a.lse_q = (float*)(ws + w.lse_q);
   a.qm_mass = chunk_score ? (float*)(ws + w.qm_mass) : nullptr;
+  a.km_part = (float*)(ws + w.km_part);
   a.B = d->batch;
   a.N = d->n_chunks;
   a.C = d->chunk_len;
@@ -310,7 +319,8 @@ pd_status pd_prefill_chunks(const pd_dims* d, const void* q_pre, const void* k_p
     if (err != hipSuccess) return hip_status(err, "prefill kernel");
     err = pd::launch_escore_bf16(e, d->head_dim, s);
     if (err != hipSuccess) return hip_status(err, "token-score kernel");
-    err = pd::launch_head_sum_rank(a.part_i, tok_score, tok_rank, a.B, a.N, a.Hq, a.C, s);
+    err = pd::launch_head_sum_rank(a.part_i, tok_score, tok_rank, a.B, a.N, a.Hq, a.C, a.km_part, key_mean, a.Hkv,
+                                   d->head_dim, km_slots(d), s);
     if (err != hipSuccess) return hip_status(err, "token-rank kernel");
   } else {
     err = pd::launch_prefill_f32(a, d->head_dim, s);
@@ -321,13 +331,14 @@ pd_status pd_prefill_chunks(const pd_dims* d, const void* q_pre, const void* k_p
     if (err != hipSuccess) return hip_status(err, "token-score kernel");
     err = pd::launch_token_rank(tok_score, tok_rank, a.B, a.N, a.C, s);
     if (err != hipSuccess) return hip_status(err, "token-rank kernel");
+    err = pd::launch_key_mean(k_cache, key_mean, a.B, a.N, a.C, a.Hkv, d->head_dim, false, s);
+    if (err != hipSuccess) return hip_status(err, "key-mean kernel");
   }
   if (chunk_score) {
     err = pd::launch_chunk_score(a.qm_mass, chunk_score, a.B, a.N, a.Hq, a.Lq, a.Lm, s);
     if (err != hipSuccess) return hip_status(err, "chunk-score kernel");
   }
-  err = pd::launch_key_mean(k_cache, key_mean, a.B, a.N, a.C, a.Hkv, d->head_dim, bf16, s);
-  return hip_status(err, "key-mean kernel");
+  return ok();
 }
 
 pd_status pd_select_ranked(const pd_dims* d, int32_t top_k, int32_t tok_budget, const float* chunk_score,

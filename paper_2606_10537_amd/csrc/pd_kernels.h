@@ -36,6 +36,7 @@ struct PrefillArgs {
   float* part_i;   // [B][N][Hq][C]  per-head mass of content row j on the query columns
   float* lse_q;    // [B][N][Hq][Lq] log2-domain LSE of the query rows
   float* qm_mass;  // [B][N][Hq][Lq+Lm] mass of each q/m row on the C content columns, or nullptr
+  float* km_part;  // bf16: [B][N][Hkv][n_qt*G][d] content-key sums of each cache-writing workgroup
   int B, N, C, Lq, Lm, Hq, Hkv, G, Sc;
   int n_qt, n_kvt, total;
   int qm_per_chunk;
@@ -118,7 +119,8 @@ hipError_t launch_gather_joint(const JointArgs& a, hipStream_t s);
 hipError_t launch_token_rank(const float* tok_score, int32_t* tok_rank, int B, int N, int C, hipStream_t s);
 // e = sum over the H_q heads of the per-head sums (fixed order), then the ranks.
 hipError_t launch_head_sum_rank(const float* per_head, float* tok_score, int32_t* tok_rank, int B, int N, int Hq,
-                                int C, hipStream_t s);
+                                int C, const float* km_part, float* key_mean, int Hkv, int D, int km_slots,
+                                hipStream_t s);
 hipError_t launch_chunk_score(const float* qm_mass, float* chunk_score, int B, int N, int Hq, int Lq, int Lm,
                               hipStream_t s);
 hipError_t launch_select_ranked(const float* chunk_score, int lowest, const int32_t* tok_rank, int32_t* chunk_idx,

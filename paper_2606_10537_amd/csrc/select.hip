@@ -122,10 +122,21 @@ __global__ __launch_bounds__(256) void token_rank_kernel(const float* tok_score,
 
 // e of one chunk = sum over the H_q heads of the per-head sums (heads in
 // ascending order), written out, then every token's rank as token_rank_kernel.
+// It also finishes the chunk's key means: k-bar[g][d] = (1/C) * the sum of the
+// km_slots partial sums of the cache-writing workgroups (fixed order).
 __global__ __launch_bounds__(256) void head_sum_rank_kernel(const float* per_head, float* tok_score,
-                                                             int32_t* tok_rank, int Hq, int C, int Cpad) {
+                                                             int32_t* tok_rank, int Hq, int C, int Cpad,
+                                                             const float* km_part, float* key_mean, int HD,
+                                                             int D, int km_slots) {
   extern __shared__ __attribute__((aligned(16))) uint64_t keys[];
   const size_t bn = blockIdx.x;
+  for (int i = threadIdx.x; i < HD; i += 256) {
+    const int g = i / D, d = i % D;
+    const float* src = km_part + ((bn * (HD / D) + g) * (size_t)km_slots) * D + d;
+    float sum = 0.f;
+    for (int q = 0; q < km_slots; ++q) sum += src[(size_t)q * D];
+    key_mean[bn * HD + i] = sum * (1.0f / C);
+  }
   const float* ph = per_head + bn * Hq * C;
   for (int j = threadIdx.x; j < Cpad; j += 256) {
     if (j < C) {
@@ -144,10 +155,11 @@ __global__ __launch_bounds__(256) void head_sum_rank_kernel(const float* per_hea
 }
 
 hipError_t launch_head_sum_rank(const float* per_head, float* tok_score, int32_t* tok_rank, int B, int N, int Hq,
-                                int C, hipStream_t s) {
+                                int C, const float* km_part, float* key_mean, int Hkv, int D, int km_slots,
+                                hipStream_t s) {
   const int Cpad = next_pow2(C);
   hipLaunchKernelGGL(head_sum_rank_kernel, dim3(B * N), dim3(256), (size_t)Cpad * 8, s, per_head, tok_score, tok_rank,
-                     Hq, C, Cpad);
+                     Hq, C, Cpad, km_part, key_mean, Hkv * D, D, km_slots);
   return hipGetLastError();
 }
 
