@@ -91,7 +91,8 @@ def test_chunk_score_parity(case):
     np.testing.assert_allclose(h64(out["chunk_score"]), s_ref, rtol=0, atol=SCORE_ATOL)
 
 
-@pytest.mark.parametrize("case", [CASES[0], CASES[2], CASES[4]], ids=["bf16-small", "bf16-tiles", "fp32"])
+@pytest.mark.parametrize("case", [CASES[0], CASES[2], CASES[4], (PD_BF16, 1, 2, 96, 200, 10, 4, 2, 128, 0)],
+                         ids=["bf16-small", "bf16-tiles", "fp32", "bf16-200-query-rows"])
 def test_query_to_chunk_token_score(case):
     dt, B, N, C, Lq, Lm, Hq, Hkv, D, pc = case
     d = Dims(B, N, C, Lq, Lm, 8, Hq, Hkv, D, dt, 0.0, pc, tok_score_dir=1)

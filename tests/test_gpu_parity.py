@@ -89,6 +89,8 @@ PREFILL_CASES = [
     (PD_BF16, 2, 2, 200, 40, 0, 6, 1, 128, 1),
     (PD_BF16, 1, 3, 64, 64, 63, 2, 2, 64, 0),
     (PD_BF16, 1, 1, 1, 1, 0, 1, 1, 128, 0),
+    (PD_BF16, 1, 2, 96, 200, 10, 7, 1, 128, 0),        # L_q > 128: several query-row passes; 7 heads per KV head
+    (PD_BF16, 1, 2, 33, 300, 0, 4, 4, 64, 1),          # L_q > 256, d = 64, per-chunk q/m rows
     (PD_BF16 + 10, 1, 2, 130, 20, 9, 4, 2, 128, 0),     # bf16 inputs, fp32 outputs
     (PD_FP32, 1, 4, 128, 16, 32, 4, 4, 64, 0),
     (PD_FP32, 2, 2, 77, 9, 3, 4, 2, 128, 1),
