@@ -1,0 +1,51 @@
+"""The command-line contract of bench.py: one JSON line with the fields the
+benchmark record needs, a roofline object consistent with itself, the oracle's
+CPU baseline, and a refusal (with a message, before any GPU work) of a
+multi-GPU run."""
+
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def run_bench(*args, timeout=300):
+    return subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *args], cwd=ROOT, capture_output=True,
+                          text=True, timeout=timeout)
+
+
+def test_bench_refuses_several_gpus():
+    r = run_bench("--gpus", "2", timeout=120)
+    assert r.returncode != 0
+    assert "one GPU" in r.stdout + r.stderr
+    assert not any(line.startswith("{") for line in r.stdout.splitlines())
+
+
+@pytest.mark.gpu
+def test_bench_json_line():
+    print("[bench contract] workload 2, 1 step, no warmup", flush=True)
+    r = run_bench("--workload", "2", "--steps", "1", "--warmup", "0", "--cpu-seconds", "1", "--no-static",
+                  "--no-achievable")
+    assert r.returncode == 0, r.stderr[-2000:]
+    lines = [line for line in r.stdout.splitlines() if line.startswith("{")]
+    assert len(lines) == 1, r.stdout
+    d = json.loads(lines[0])
+    for key in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better",
+                "scaling", "vs_baseline", "dtype", "data", "config", "roofline", "cpu_baseline"):
+        assert key in d, key
+    assert d["n_gpus"] == 1 and d["steps"] == 1 and d["warmup"] == 0
+    assert d["value"] > 0 and d["ms_per_step"] > 0 and d["higher_is_better"] is True
+    assert d["vs_baseline"] is None and d["data"] == "synthetic" and d["dtype"] == "bf16"
+    assert "workload" in d["config"]
+    roof = d["roofline"]
+    assert roof["bound"] in ("hbm", "mfma", "alu") and roof["unit"] in ("GB/s", "TFLOP/s")
+    assert roof["peak"] > 0 and roof["achieved"] > 0
+    assert abs(roof["frac"] - roof["achieved"] / roof["peak"]) <= 1e-3 * roof["frac"] + 1e-4
+    assert "traffic" in roof
+    cpu = d["cpu_baseline"]
+    assert cpu["kind"] == "oracle" and cpu["value"] > 0 and cpu["cores"] >= 1
+    assert cpu["unit"] == d["unit"] and cpu["sample"]
