@@ -214,3 +214,39 @@ def test_binding_raises_on_error():
     with pytest.raises(PdError) as ei:
         _lib._check(2)
     assert ei.value.status == 2
+
+
+def test_error_message_is_thread_local(lib):
+    """Each thread reads the message of its own last failure, whatever another
+    thread failed with in between."""
+    import threading
+    bar = threading.Barrier(2)
+    out = {}
+
+    def first():
+        try:
+            out["a_status"] = prefill(dims(), q_pre=None)
+            bar.wait()
+            bar.wait()
+            out["a"] = lib.pd_last_error_message()
+        except Exception as e:   # reported below
+            out["a_err"] = e
+
+    def second():
+        try:
+            bar.wait()
+            out["b_status"] = prefill(dims(batch=0))
+            out["b"] = lib.pd_last_error_message()
+            bar.wait()
+        except Exception as e:
+            out["b_err"] = e
+
+    ts = [threading.Thread(target=first), threading.Thread(target=second)]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join(30)
+    assert "a_err" not in out and "b_err" not in out, out
+    assert out["a_status"] == 1 and out["b_status"] == 2
+    assert b"q_pre" in out["a"] and b"batch" not in out["a"]
+    assert b"batch" in out["b"]
