@@ -21,6 +21,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA (published)
+PEAK_FP32_TFLOPS = 157.3       # MI355X fp32 vector (published; the fp32 path runs on VALU FMAs)
 PEAK_HBM_GBPS = 8000.0         # MI355X HBM3E (published)
 
 
@@ -478,20 +479,24 @@ def main():
     dec_tflops = dec_flop / (dec_kern_ms * 1e-3) / 1e12
     dec_gbps = dec_bytes / (dec_kern_ms * 1e-3) / 1e9
     pre_tflops = pre_flop / (pre_ms_layer * 1e-3) / 1e12
-    ridge = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBPS * 1e9)
-    dec_bound = "mfma" if dec_flop / dec_bytes > ridge else "hbm"
-    if dec_bound == "mfma":
-        roof = {"bound": "mfma", "achieved": round(dec_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(dec_tflops / PEAK_BF16_TFLOPS, 4)}
+    bf16 = w.dtype == _lib.PD_BF16
+    peak_c = PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS
+    ridge = peak_c * 1e12 / (PEAK_HBM_GBPS * 1e9)
+    dec_bound = ("mfma" if bf16 else "alu") if dec_flop / dec_bytes > ridge else "hbm"
+    if dec_bound != "hbm":
+        roof = {"bound": dec_bound, "achieved": round(dec_tflops, 2), "peak": peak_c, "unit": "TFLOP/s",
+                "frac": round(dec_tflops / peak_c, 4)}
     else:
         roof = {"bound": "hbm", "achieved": round(dec_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                 "frac": round(dec_gbps / PEAK_HBM_GBPS, 4)}
-    roof.update({"kernel": "decode_bf16_kernel<128> (pd_sparse_decode_attn, one launch per layer and step)",
+    kname = f"decode_{'bf16' if bf16 else 'f32'}_kernel<{D}>"
+    roof.update({"kernel": f"{kname} (pd_sparse_decode_attn, one launch per layer and step)",
                  "traffic": measured_traffic() if (args.workload == 5 and not args.layers) else None,
                  "launch_ms": round(dec_kern_ms, 5), "flop_per_launch": dec_flop,
                  "bytes_per_launch": dec_bytes})
 
     traffic = roof.get("traffic")
+    ctx = f"{w.context // 1024}K" if w.context >= 1024 else f"{w.context}-token"
     res = {
         "metric": "denoising steps/sec + decode-attn HBM GB/s + prefill MFMA TFLOP/s at 32K",
         "value": round(T / (ms * 1e-3), 3),
@@ -499,8 +504,8 @@ def main():
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms, 3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": f"{w.context // 1024}K context ({w.name}): B={B}, layers={L}, N={N}, C={C}, "
+        "dtype": "bf16" if bf16 else "f32", "data": "synthetic",
+        "config": {"workload": f"{ctx} context ({w.name}): B={B}, layers={L}, N={N}, C={C}, "
                                f"L_q={w.q_len}, L_m={w.m_len}, L_d={Ld}, H_q/H_kv={Hq}/{Hkv}, d={D}, K={K}, "
                                f"B_tok={Bt}, T={T}",
                    "global_batch": B, "seq_len": w.context, "parallelism": "single GPU",
@@ -511,9 +516,10 @@ def main():
         "decode_attn_tflops": round(dec_tflops, 2),
         "prefill_ms_per_layer": round(pre_ms_layer, 3),
         "prefill_tflops": round(pre_tflops, 2),
-        "prefill_mfma_frac": round(pre_tflops / PEAK_BF16_TFLOPS, 4),
+        "prefill_mfma_frac": round(pre_tflops / peak_c, 4),
+        "compute_peak_tflops": peak_c,
         "decode_dram_gbps": round(traffic / (dec_kern_ms * 1e-3) / 1e9, 1) if traffic else None,
-        "decode_binding_roof_frac": round(max(dec_flop / (PEAK_BF16_TFLOPS * 1e12), dec_bytes / (PEAK_HBM_GBPS * 1e9))
+        "decode_binding_roof_frac": round(max(dec_flop / (peak_c * 1e12), dec_bytes / (PEAK_HBM_GBPS * 1e9))
                                           / (dec_kern_ms * 1e-3), 4),
         "cold_flush_mib": args.flush_mib,
         "roofline": roof,
@@ -530,9 +536,11 @@ def main():
     if not args.no_achievable:
         ach = achievable_peaks(torch, dev)
         res["achievable"] = ach
-        roof["frac_of_achievable"] = round(roof["achieved"] / (ach["mfma_tflops"] if roof["bound"] == "mfma"
-                                                               else ach["hbm_gbps"]), 4)
-        res["prefill_frac_of_achievable"] = round(pre_tflops / ach["mfma_tflops"], 4)
+        if roof["bound"] != "alu":   # the achievable rates are bf16 MFMA and HBM
+            roof["frac_of_achievable"] = round(roof["achieved"] / (ach["mfma_tflops"] if roof["bound"] == "mfma"
+                                                                   else ach["hbm_gbps"]), 4)
+        if bf16:
+            res["prefill_frac_of_achievable"] = round(pre_tflops / ach["mfma_tflops"], 4)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
