@@ -39,7 +39,7 @@ def draw(i):
                 splits=int(rng.choice([0, 1, 3])))
 
 
-@pytest.mark.parametrize("i", range(24))
+@pytest.mark.parametrize("i", range(48))
 def test_random_shape_path(i):
     c = draw(i)
     print(f"[sweep {i}] {c}", flush=True)
