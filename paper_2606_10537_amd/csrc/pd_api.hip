@@ -112,8 +112,7 @@ PrefillWs prefill_ws(const pd_dims* d) {
 // row sets a selection averages (L_d decode rows, or L_m pseudo-label rows).
 size_t select_ws(const pd_dims* d) {
   const int rows = std::max(d->dec_len, std::max(d->m_len, 1));
-  return round_up((size_t)d->batch * d->n_chunks * d->n_heads_q *
-                  pd::select_row_splits(d->batch, d->n_heads_q, rows) * sizeof(float));
+  return round_up((size_t)d->batch * d->n_chunks * d->n_heads_q * pd::select_row_splits(rows) * sizeof(float));
 }
 
 int decode_qtiles(const pd_dims* d) {
@@ -397,8 +396,7 @@ pd_status pd_score_select(const pd_dims* d, int32_t top_k, int32_t tok_budget, c
   a.q_rows = d->dec_len;
   a.q_row0 = 0;
   a.q_bstride = d->dec_len;
-  a.NS = pd::select_row_splits(a.B, a.Hq, a.q_rows);
-  a.rps = (a.q_rows + a.NS - 1) / a.NS;
+  a.NS = pd::select_row_splits(a.q_rows);
   a.bf16 = d->dtype == PD_BF16;
   a.scale = scale_of(d);
   return hip_status(pd::launch_score_select(a, (hipStream_t)stream), "score/select kernels");
@@ -445,8 +443,7 @@ pd_status pd_score_select_static(const pd_dims* d, int32_t top_k, int32_t tok_bu
   a.q_rows = d->m_len;
   a.q_row0 = d->q_len;
   a.q_bstride = (d->qm_per_chunk ? d->n_chunks : 1) * (d->q_len + d->m_len);
-  a.NS = pd::select_row_splits(a.B, a.Hq, a.q_rows);
-  a.rps = (a.q_rows + a.NS - 1) / a.NS;
+  a.NS = pd::select_row_splits(a.q_rows);
   a.bf16 = d->dtype == PD_BF16;
   a.scale = scale_of(d);
   return hip_status(pd::launch_score_select(a, (hipStream_t)stream), "static score/select kernels");

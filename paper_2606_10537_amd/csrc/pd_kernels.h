@@ -97,7 +97,6 @@ struct SelectArgs {
   int32_t *chunk_idx, *tok_slot;
   int B, N, C, Hq, Hkv, G, Ld, D, K, Bt, NS;
   int q_rows, q_row0, q_bstride;   // rows averaged into the mean query: rows q_row0.. of q_bstride per sequence
-  int rps;                         // rows per split: split sp takes rows sp*rps .. of the q_rows
   bool bf16;
   float scale;
 };
@@ -126,6 +125,6 @@ hipError_t launch_chunk_score(const float* qm_mass, float* chunk_score, int B, i
                               hipStream_t s);
 hipError_t launch_select_ranked(const float* chunk_score, int lowest, const int32_t* tok_rank, int32_t* chunk_idx,
                                 int32_t* tok_slot, int B, int N, int C, int K, int Bt, hipStream_t s);
-int select_row_splits(int B, int Hq, int rows);
+int select_row_splits(int Ld);
 
 }  // namespace pd

@@ -169,22 +169,11 @@ hipError_t launch_token_rank(const float* tok_score, int32_t* tok_rank, int B, i
   return hipGetLastError();
 }
 
-// Row splits of the chunk-score terms: about one workgroup per CU over the
-// B*H_q (sequence, head) pairs (one split when they fill the chip, as at
-// batch 8 with 32 heads; more for small batches), at least 32 rows and at most
-// kScoreRowsMax rows per workgroup.
-#ifndef PD_SCORE_TARGET_WG
-#define PD_SCORE_TARGET_WG 256
-#endif
-constexpr int kScoreRowsMax = 512;
-int select_row_splits(int B, int Hq, int rows) {
-  const int pairs = std::max(1, B * Hq);
-  const int by_grid = std::max(1, PD_SCORE_TARGET_WG / pairs);
-  const int by_rows = std::max(1, (rows + 31) / 32);
-  return std::max((rows + kScoreRowsMax - 1) / kScoreRowsMax, std::min(by_grid, by_rows));
-}
+// Decode rows per score workgroup.
+constexpr int kScoreRows = 128;
+int select_row_splits(int Ld) { return (Ld + kScoreRows - 1) / kScoreRows; }
 
-// Chunk-score terms of one (b, h, row split of rps rows): scale * <(1/L_d) sum_r q_r, kbar[b][n][h/G]> for all n.
+// Chunk-score terms of one (b, h, row split): scale * <(1/L_d) sum_r q_r, kbar[b][n][h/G]> for all n.
 // Latency-bound (a few KB per workgroup), so every load of a thread is issued
 // before the first use: the key means of the first 32 chunks, then the thread's
 // share of the rows (fully unrolled).  The row sums are reduced through LDS in
@@ -193,10 +182,10 @@ int select_row_splits(int B, int Hq, int rows) {
 template <bool BF16, int D>
 __global__ __launch_bounds__(256) void qscore_kernel(const void* q_dec, const float* key_mean, float* partial,
                                                       int N, int Hq, int Hkv, int G, int rows, int row0, int bstride,
-                                                      int NS, int rps, float scale) {
+                                                      int NS, float scale) {
   constexpr int SL = D / 8;
   constexpr int E = Vec16<BF16>::E;
-  constexpr int TPR = D / E, NG = 256 / TPR, IT = kScoreRowsMax / NG;
+  constexpr int TPR = D / E, NG = 256 / TPR, IT = kScoreRows / NG;
   __shared__ float red[NG * D];
   __shared__ float qp[D];
   // Heads fastest: workgroups that run together read whole contiguous rows.
@@ -204,7 +193,7 @@ __global__ __launch_bounds__(256) void qscore_kernel(const void* q_dec, const fl
   const int sp = (blockIdx.x / Hq) % NS;
   const int b = blockIdx.x / (Hq * NS);
   const int t = threadIdx.x;
-  const int r0 = sp * rps, nr = min(rows, r0 + rps) - r0;
+  const int r0 = sp * kScoreRows, nr = min(rows, r0 + kScoreRows) - r0;
   const float* kb = key_mean + ((size_t)b * N * Hkv + h / G) * D;
   const int j = t & 7;
   f32x4 kv[SL / 4];
@@ -370,7 +359,7 @@ hipError_t launch_score_select(const SelectArgs& a, hipStream_t s) {
   const dim3 g1(a.B * a.Hq * a.NS);
 #define PD_QSCORE(BF, DD)                                                                                      \
   hipLaunchKernelGGL((qscore_kernel<BF, DD>), g1, dim3(256), 0, s, a.q_dec, a.key_mean, a.partial, a.N, a.Hq, \
-                     a.Hkv, a.G, a.q_rows, a.q_row0, a.q_bstride, a.NS, a.rps, a.scale)
+                     a.Hkv, a.G, a.q_rows, a.q_row0, a.q_bstride, a.NS, a.scale)
   if (a.D == 128) {
     if (a.bf16) PD_QSCORE(true, 128); else PD_QSCORE(false, 128);
   } else {
