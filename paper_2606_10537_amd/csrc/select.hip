@@ -120,25 +120,54 @@ __global__ __launch_bounds__(256) void token_rank_kernel(const float* tok_score,
   for (int i = threadIdx.x; i < C; i += 256) tok_rank[bn * C + (uint32_t)keys[i]] = i;
 }
 
-// e of one chunk = sum over the H_q heads of the per-head sums (heads in
-// ascending order), written out, then every token's rank as token_rank_kernel.
-// It also finishes the chunk's key means: k-bar[g][d] = (1/C) * the sum of the
-// km_slots partial sums of the cache-writing workgroups (fixed order).
-__global__ __launch_bounds__(256) void head_sum_rank_kernel(const float* per_head, float* tok_score,
-                                                             int32_t* tok_rank, int Hq, int C, int Cpad,
-                                                             const float* km_part, float* key_mean, int HD,
-                                                             int D, int km_slots) {
+// Ascending bitonic sort of P (power of two) keys in LDS by NT threads.
+template <int NT>
+__device__ void bitonic_sort_nt(uint64_t* keys, int P) {
+  for (int k = 2; k <= P; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = threadIdx.x; i < P; i += NT) {
+        const int ixj = i ^ j;
+        if (ixj > i) {
+          const uint64_t a = keys[i], c = keys[ixj];
+          const bool up = (i & k) == 0;
+          if ((a > c) == up) {
+            keys[i] = c;
+            keys[ixj] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// Workgroups (b*N + n, 0): e of one chunk = sum over the H_q heads of the
+// per-head sums (heads in ascending order), written out, then every token's
+// rank as token_rank_kernel, with 1024 threads (one compare per thread per
+// sort stage at C = 1024).  Workgroups (b*N + n, y >= 1): the chunk's key means
+// k-bar[g][d] = (1/C) * the sum of the km_slots partial sums of the
+// cache-writing workgroups (fixed order); these workgroups (at most 64 per
+// chunk) take 1024 of the H_kv*d values at a time.
+constexpr int kRankThreads = 1024;
+__global__ __launch_bounds__(kRankThreads) void head_sum_rank_kernel(const float* per_head, float* tok_score,
+                                                                      int32_t* tok_rank, int Hq, int C, int Cpad,
+                                                                      const float* km_part, float* key_mean, int HD,
+                                                                      int D, int km_slots) {
   extern __shared__ __attribute__((aligned(16))) uint64_t keys[];
   const size_t bn = blockIdx.x;
-  for (int i = threadIdx.x; i < HD; i += 256) {
-    const int g = i / D, d = i % D;
-    const float* src = km_part + ((bn * (HD / D) + g) * (size_t)km_slots) * D + d;
-    float sum = 0.f;
-    for (int q = 0; q < km_slots; ++q) sum += src[(size_t)q * D];
-    key_mean[bn * HD + i] = sum * (1.0f / C);
+  if (blockIdx.y > 0) {
+    for (int i = (blockIdx.y - 1) * kRankThreads + threadIdx.x; i < HD; i += (gridDim.y - 1) * kRankThreads) {
+      const int g = i / D, d = i % D;
+      const float* src = km_part + ((bn * (HD / D) + g) * (size_t)km_slots) * D + d;
+      float sum = 0.f;
+#pragma unroll 8
+      for (int q = 0; q < km_slots; ++q) sum += src[(size_t)q * D];
+      key_mean[bn * HD + i] = sum * (1.0f / C);
+    }
+    return;
   }
   const float* ph = per_head + bn * Hq * C;
-  for (int j = threadIdx.x; j < Cpad; j += 256) {
+  for (int j = threadIdx.x; j < Cpad; j += kRankThreads) {
     if (j < C) {
       float e = 0.f;
 #pragma unroll 16
@@ -150,16 +179,18 @@ __global__ __launch_bounds__(256) void head_sum_rank_kernel(const float* per_hea
     }
   }
   __syncthreads();
-  bitonic_sort(keys, Cpad);
-  for (int i = threadIdx.x; i < C; i += 256) tok_rank[bn * C + (uint32_t)keys[i]] = i;
+  bitonic_sort_nt<kRankThreads>(keys, Cpad);
+  for (int i = threadIdx.x; i < C; i += kRankThreads) tok_rank[bn * C + (uint32_t)keys[i]] = i;
 }
 
 hipError_t launch_head_sum_rank(const float* per_head, float* tok_score, int32_t* tok_rank, int B, int N, int Hq,
                                 int C, const float* km_part, float* key_mean, int Hkv, int D, int km_slots,
                                 hipStream_t s) {
   const int Cpad = next_pow2(C);
-  hipLaunchKernelGGL(head_sum_rank_kernel, dim3(B * N), dim3(256), (size_t)Cpad * 8, s, per_head, tok_score, tok_rank,
-                     Hq, C, Cpad, km_part, key_mean, Hkv * D, D, km_slots);
+  const int HD = Hkv * D;
+  const dim3 grid(B * N, 1 + std::min(64, (HD + kRankThreads - 1) / kRankThreads));
+  hipLaunchKernelGGL(head_sum_rank_kernel, grid, dim3(kRankThreads), (size_t)Cpad * 8, s, per_head, tok_score,
+                     tok_rank, Hq, C, Cpad, km_part, key_mean, HD, D, km_slots);
   return hipGetLastError();
 }
 
