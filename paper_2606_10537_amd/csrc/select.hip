@@ -616,15 +616,36 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* o_part, const f
   const size_t row = gid / TPR;
   if (row >= rows) return;
   const int c = gid % TPR;
+  // Shards in groups of 8 whose loads are all issued before the first use
+  // (the shard count is a run-time value); summed in ascending shard order.
+  constexpr int U = 8;
   float M = -INFINITY;
-  for (int sp = 0; sp < S; ++sp) M = fmaxf(M, lse_part[sp * rows + row]);
+  for (int s0 = 0; s0 < S; s0 += U) {
+    float l[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) l[u] = s0 + u < S ? lse_part[(s0 + u) * rows + row] : -INFINITY;
+#pragma unroll
+    for (int u = 0; u < U; ++u) M = fmaxf(M, l[u]);
+  }
   float W = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  for (int sp = 0; sp < S; ++sp) {
-    const float w = fast_exp2(lse_part[sp * rows + row] - M);
-    W += w;
-    const f32x4 v = *reinterpret_cast<const f32x4*>(o_part + (sp * rows + row) * D + 4 * c);
-    acc += w * v;
+  for (int s0 = 0; s0 < S; s0 += U) {
+    float l[U];
+    f32x4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const bool in = s0 + u < S;
+      l[u] = in ? lse_part[(s0 + u) * rows + row] : 0.f;
+      v[u] = in ? *reinterpret_cast<const f32x4*>(o_part + ((s0 + u) * rows + row) * D + 4 * c) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (s0 + u < S) {
+        const float w = fast_exp2(l[u] - M);
+        W += w;
+        acc += w * v[u];
+      }
+    }
   }
   const float inv = 1.0f / W;
   // row = (b*Hq + h)*Ld + r  ->  o_dec[b][r][h][:]
