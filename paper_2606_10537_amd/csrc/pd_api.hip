@@ -155,6 +155,19 @@ int effective_splits(const pd_dims* d, long long n_sel, int n_static, int num_sp
 
 long long n_sel_of(int top_k, int tok_budget) { return (long long)top_k * (1 + tok_budget); }
 
+// The decode kernels address the static and own rows of a (sequence, KV head)
+// as row * H_kv * d from a base shifted back by the prefix rows, in 32-bit
+// element offsets: every KV row index of one call, times H_kv * d, must stay
+// below 2^31.
+pd_status check_decode_rows(const pd_dims* d, long long n_sel, long long n_static) {
+  const long long rows = n_sel + n_static + d->dec_len;
+  if (rows * d->n_heads_kv * d->head_dim >= (1LL << 31))
+    return fail(PD_ERR_BAD_DIMS,
+                "decode KV rows (n_sel=%lld + n_static=%lld + dec_len=%d) * n_heads_kv * head_dim must stay below 2^31",
+                n_sel, n_static, d->dec_len);
+  return PD_OK;
+}
+
 size_t decode_ws_bytes(const pd_dims* d, int S) {
   if (S <= 1) return 0;
   const size_t rows = (size_t)S * d->batch * d->n_heads_q * d->dec_len;
@@ -227,6 +240,7 @@ size_t pd_workspace_bytes(const pd_dims* d, int32_t top_k, int32_t tok_budget, i
     case 1: return select_ws(d);
     case 2:
       if (top_k < 1 || tok_budget < 1 || num_splits < 0 || num_splits > kMaxSplits) return 0;
+      if (check_decode_rows(d, n_sel_of(top_k, tok_budget), 0) != PD_OK) return 0;
       return decode_ws_bytes(d, requested_splits(d, n_sel_of(top_k, tok_budget), num_splits));
     default: return 0;
   }
@@ -554,6 +568,7 @@ static pd_status decode_core(const pd_dims* d, int top_k, int tok_budget, long l
     PD_REQUIRE_PTR(v_static);
   }
   if (lse_dec && !aligned16(lse_dec)) return fail(PD_ERR_MISALIGNED, "pointer 'lse_dec' is not 16-byte aligned");
+  PD_RETURN_IF(check_decode_rows(d, n_sel, n_static));
   const int S_req = requested_splits(d, n_sel, num_splits);
   const int S = effective_splits(d, n_sel, n_static, num_splits);
   PD_RETURN_IF(check_ws(workspace, ws_bytes, decode_ws_bytes(d, S_req)));
@@ -643,6 +658,7 @@ pd_status pd_sparse_decode_attn_compact(const pd_dims* d, int32_t n_sel, const v
 size_t pd_compact_workspace_bytes(const pd_dims* d, int32_t n_sel, int32_t num_splits) {
   if (check_dims(d) != PD_OK || n_sel < 0 || n_sel > kMaxCompactRows || num_splits < 0 || num_splits > kMaxSplits)
     return 0;
+  if (check_decode_rows(d, n_sel, 0) != PD_OK) return 0;
   return decode_ws_bytes(d, requested_splits(d, n_sel, num_splits));
 }
 

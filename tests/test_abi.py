@@ -148,6 +148,27 @@ def test_static_mode_validation(lib):
     assert _lib.pd_compact_workspace_bytes(d, 100, 3) >= 3 * 1 * 4 * 32 * 65 * 4
 
 
+def test_decode_row_offsets_bounded(lib):
+    """A decode whose KV row index times H_kv * d reaches 2^31 is rejected on the host (the kernels
+    address static and own rows with 32-bit element offsets), for both decode entry points and the
+    size queries; nothing is launched."""
+    d = dims(n_heads_q=32, n_heads_kv=32, head_dim=128, q_len=16, m_len=32, dec_len=32)
+    c = ctypes.byref(d.c())
+    n_sel = 1 << 20
+    assert (n_sel + 16 + 32) * 32 * 128 >= 1 << 31
+    st = lib.pd_sparse_decode_attn_compact(c, n_sel, A, A, A, A, A, A, A, 16, A, None, 0, A, 1 << 40, None)
+    assert st == 2
+    assert b"2^31" in lib.pd_last_error_message()
+    assert _lib.pd_compact_workspace_bytes(d, n_sel, 0) == 0
+    # the gathered entry point: K * (1 + B_tok) prefix rows over the same bound
+    dg = dims(n_heads_q=32, n_heads_kv=32, head_dim=128, n_chunks=1024, chunk_len=4096, q_len=16, m_len=32,
+              dec_len=32)
+    assert _lib.pd_workspace_bytes(dg, 1024, 4096, 0, 2) == 0
+    # one sequence's cache alone already exceeds the per-sequence bound of check_dims here
+    assert lib.pd_sparse_decode_attn(ctypes.byref(dg.c()), 1024, 4096, A, A, A, A, A, A, A, A, A, 16, A, None,
+                                     0, A, 1 << 40, None) == 2
+
+
 def test_select_ranked_validation(lib):
     c = ctypes.byref(dims().c())
     call = lambda k=2, bt=64, cs=A, low=1, tr=A, ci=A, dd=c: lib.pd_select_ranked(dd, k, bt, cs, low, tr, ci, A, None)
