@@ -153,7 +153,7 @@ def static_mode(torch, _lib, w, d, pool, dec_pool, k_cache, v_cache, key_mean, t
     B, Hkv, D = w.batch, w.n_heads_kv, w.head_dim
     n_sel = K * (1 + Bt)
     sh = stream.cuda_stream
-    ws_sel = torch.empty(_lib.pd_workspace_bytes(d, K, Bt, 0, 1), dtype=torch.uint8, device=dev)
+    ws_sel = torch.zeros(_lib.pd_workspace_bytes(d, K, Bt, 0, 1), dtype=torch.uint8, device=dev)
     ws_dec = torch.empty(max(16, _lib.pd_compact_workspace_bytes(d, n_sel, 0)), dtype=torch.uint8, device=dev)
     ci = torch.empty((B, K), dtype=torch.int32, device=dev)
     ts = torch.empty((B, K, Bt), dtype=torch.int32, device=dev)
@@ -401,7 +401,7 @@ def main():
     tok_rank = [torch.empty((B, N, C), dtype=torch.int32, device=dev) for _ in range(L)]
     key_mean = [torch.empty((B, N, Hkv, D), dtype=torch.float32, device=dev) for _ in range(L)]
     ws_pre = torch.empty(_lib.pd_workspace_bytes(d, which=0), dtype=torch.uint8, device=dev)
-    ws_sel = torch.empty(_lib.pd_workspace_bytes(d, K, Bt, 0, 1), dtype=torch.uint8, device=dev)
+    ws_sel = torch.zeros(_lib.pd_workspace_bytes(d, K, Bt, 0, 1), dtype=torch.uint8, device=dev)
     ws_dec = torch.empty(max(16, _lib.pd_workspace_bytes(d, K, Bt, 0, 2)), dtype=torch.uint8, device=dev)
     chunk_idx = torch.empty((B, K), dtype=torch.int32, device=dev)
     tok_slot = torch.empty((B, K, Bt), dtype=torch.int32, device=dev)

@@ -373,46 +373,66 @@ pd_status pd_select_ranked(const pd_dims* d, int32_t top_k, int32_t tok_budget, 
                     "select kernel");
 }
 
-pd_status pd_score_select(const pd_dims* d, int32_t top_k, int32_t tok_budget, const void* q_dec,
-                          const float* key_mean, const int32_t* tok_rank, int32_t* chunk_idx, int32_t* tok_slot,
-                          float* chunk_score, void* workspace, size_t ws_bytes, void* stream) {
-  PD_RETURN_IF(check_dims(d));
+}  // extern "C"
+
+namespace {
+
+// Shared by the selection entry points: sizes and pointers checked here, the
+// mean query over `rows` rows starting at row0 of every bstride rows of q.
+pd_status select_args(const pd_dims* d, int32_t top_k, int32_t tok_budget, const void* q, const float* key_mean,
+                      const int32_t* tok_rank, int32_t* chunk_idx, int32_t* tok_slot, float* chunk_score,
+                      pd::SelectArgs* a) {
   if (top_k < 1 || top_k > d->n_chunks)
     return fail(PD_ERR_BAD_DIMS, "top_k=%d must be in 1..n_chunks=%d", top_k, d->n_chunks);
   if (tok_budget < 1 || tok_budget > d->chunk_len)
     return fail(PD_ERR_BAD_DIMS, "tok_budget=%d must be in 1..chunk_len=%d", tok_budget, d->chunk_len);
-  PD_REQUIRE_PTR(q_dec);
+  PD_REQUIRE_PTR(q);
   PD_REQUIRE_PTR(key_mean);
   PD_REQUIRE_PTR(tok_rank);
   PD_REQUIRE_PTR(chunk_idx);
   PD_REQUIRE_PTR(tok_slot);
   if (chunk_score && !aligned16(chunk_score))
     return fail(PD_ERR_MISALIGNED, "pointer 'chunk_score' is not 16-byte aligned");
+  *a = pd::SelectArgs{};
+  a->q_dec = q;
+  a->key_mean = key_mean;
+  a->tok_rank = tok_rank;
+  a->chunk_score = chunk_score;
+  a->chunk_idx = chunk_idx;
+  a->tok_slot = tok_slot;
+  a->B = d->batch;
+  a->N = d->n_chunks;
+  a->C = d->chunk_len;
+  a->Hq = d->n_heads_q;
+  a->Hkv = d->n_heads_kv;
+  a->G = a->Hq / a->Hkv;
+  a->Ld = d->dec_len;
+  a->D = d->head_dim;
+  a->K = top_k;
+  a->Bt = tok_budget;
+  a->q_rows = d->dec_len;
+  a->q_row0 = 0;
+  a->q_bstride = d->dec_len;
+  a->NS = pd::select_row_splits(a->q_rows);
+  a->bf16 = d->dtype == PD_BF16;
+  a->scale = scale_of(d);
+  return PD_OK;
+}
+
+void place_select_ws(void* ws, pd::SelectArgs* a) { a->partial = (float*)ws; }
+
+}  // namespace
+
+extern "C" {
+
+pd_status pd_score_select(const pd_dims* d, int32_t top_k, int32_t tok_budget, const void* q_dec,
+                          const float* key_mean, const int32_t* tok_rank, int32_t* chunk_idx, int32_t* tok_slot,
+                          float* chunk_score, void* workspace, size_t ws_bytes, void* stream) {
+  PD_RETURN_IF(check_dims(d));
+  pd::SelectArgs a;
+  PD_RETURN_IF(select_args(d, top_k, tok_budget, q_dec, key_mean, tok_rank, chunk_idx, tok_slot, chunk_score, &a));
   PD_RETURN_IF(check_ws(workspace, ws_bytes, select_ws(d)));
-  pd::SelectArgs a{};
-  a.q_dec = q_dec;
-  a.key_mean = key_mean;
-  a.tok_rank = tok_rank;
-  a.partial = (float*)workspace;
-  a.chunk_score = chunk_score;
-  a.chunk_idx = chunk_idx;
-  a.tok_slot = tok_slot;
-  a.B = d->batch;
-  a.N = d->n_chunks;
-  a.C = d->chunk_len;
-  a.Hq = d->n_heads_q;
-  a.Hkv = d->n_heads_kv;
-  a.G = a.Hq / a.Hkv;
-  a.Ld = d->dec_len;
-  a.D = d->head_dim;
-  a.K = top_k;
-  a.Bt = tok_budget;
-  a.q_rows = d->dec_len;
-  a.q_row0 = 0;
-  a.q_bstride = d->dec_len;
-  a.NS = pd::select_row_splits(a.q_rows);
-  a.bf16 = d->dtype == PD_BF16;
-  a.scale = scale_of(d);
+  place_select_ws(workspace, &a);
   return hip_status(pd::launch_score_select(a, (hipStream_t)stream), "score/select kernels");
 }
 
@@ -422,44 +442,16 @@ pd_status pd_score_select_static(const pd_dims* d, int32_t top_k, int32_t tok_bu
                                  void* stream) {
   PD_RETURN_IF(check_dims(d));
   if (d->m_len < 1) return fail(PD_ERR_BAD_DIMS, "m_len=%d: static selection needs pseudo-label rows", d->m_len);
-  if (top_k < 1 || top_k > d->n_chunks)
-    return fail(PD_ERR_BAD_DIMS, "top_k=%d must be in 1..n_chunks=%d", top_k, d->n_chunks);
-  if (tok_budget < 1 || tok_budget > d->chunk_len)
-    return fail(PD_ERR_BAD_DIMS, "tok_budget=%d must be in 1..chunk_len=%d", tok_budget, d->chunk_len);
-  PD_REQUIRE_PTR(q_qm);
-  PD_REQUIRE_PTR(key_mean);
-  PD_REQUIRE_PTR(tok_rank);
-  PD_REQUIRE_PTR(chunk_idx);
-  PD_REQUIRE_PTR(tok_slot);
-  if (chunk_score && !aligned16(chunk_score))
-    return fail(PD_ERR_MISALIGNED, "pointer 'chunk_score' is not 16-byte aligned");
+  pd::SelectArgs a;
+  PD_RETURN_IF(select_args(d, top_k, tok_budget, q_qm, key_mean, tok_rank, chunk_idx, tok_slot, chunk_score, &a));
   PD_RETURN_IF(check_ws(workspace, ws_bytes, select_ws(d)));
-  pd::SelectArgs a{};
-  a.q_dec = q_qm;
-  a.key_mean = key_mean;
-  a.tok_rank = tok_rank;
-  a.partial = (float*)workspace;
-  a.chunk_score = chunk_score;
-  a.chunk_idx = chunk_idx;
-  a.tok_slot = tok_slot;
-  a.B = d->batch;
-  a.N = d->n_chunks;
-  a.C = d->chunk_len;
-  a.Hq = d->n_heads_q;
-  a.Hkv = d->n_heads_kv;
-  a.G = a.Hq / a.Hkv;
-  a.Ld = d->dec_len;
-  a.D = d->head_dim;
-  a.K = top_k;
-  a.Bt = tok_budget;
+  place_select_ws(workspace, &a);
   // The L_m pseudo-label rows follow the L_q query rows of each sequence's q/m
   // block (chunk 0's copy when the rows are given per chunk).
   a.q_rows = d->m_len;
   a.q_row0 = d->q_len;
   a.q_bstride = (d->qm_per_chunk ? d->n_chunks : 1) * (d->q_len + d->m_len);
   a.NS = pd::select_row_splits(a.q_rows);
-  a.bf16 = d->dtype == PD_BF16;
-  a.scale = scale_of(d);
   return hip_status(pd::launch_score_select(a, (hipStream_t)stream), "static score/select kernels");
 }
 

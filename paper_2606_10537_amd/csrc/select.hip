@@ -209,40 +209,39 @@ int select_row_splits(int Ld) { return (Ld + kScoreRows - 1) / kScoreRows; }
 // before the first use: the key means of the first 32 chunks, then the thread's
 // share of the rows (fully unrolled).  The row sums are reduced through LDS in
 // a fixed order; the dot products run 8 lanes per chunk (D/8 dimensions each),
-// reduced by a fixed xor butterfly.
+// reduced by a fixed xor butterfly.  Workgroup id: heads fastest, then row
+// split, then sequence.
 template <bool BF16, int D>
-__global__ __launch_bounds__(256) void qscore_kernel(const void* q_dec, const float* key_mean, float* partial,
-                                                      int N, int Hq, int Hkv, int G, int rows, int row0, int bstride,
-                                                      int NS, float scale) {
+__device__ __forceinline__ void qscore_terms(const SelectArgs& a, int bid) {
   constexpr int SL = D / 8;
   constexpr int E = Vec16<BF16>::E;
   constexpr int TPR = D / E, NG = 256 / TPR, IT = kScoreRows / NG;
   __shared__ float red[NG * D];
   __shared__ float qp[D];
-  // Heads fastest: workgroups that run together read whole contiguous rows.
-  const int h = blockIdx.x % Hq;
-  const int sp = (blockIdx.x / Hq) % NS;
-  const int b = blockIdx.x / (Hq * NS);
+  const int N = a.N, Hq = a.Hq, NS = a.NS;
+  const int h = bid % Hq;
+  const int sp = (bid / Hq) % NS;
+  const int b = bid / (Hq * NS);
   const int t = threadIdx.x;
-  const int r0 = sp * kScoreRows, nr = min(rows, r0 + kScoreRows) - r0;
-  const float* kb = key_mean + ((size_t)b * N * Hkv + h / G) * D;
+  const int r0 = sp * kScoreRows, nr = min(a.q_rows, r0 + kScoreRows) - r0;
+  const float* kb = a.key_mean + ((size_t)b * N * a.Hkv + h / a.G) * D;
   const int j = t & 7;
   f32x4 kv[SL / 4];
   {
     const int n = t >> 3;
     if (n < N) {
-      const f32x4* kr = reinterpret_cast<const f32x4*>(kb + (size_t)n * Hkv * D + j * SL);
+      const f32x4* kr = reinterpret_cast<const f32x4*>(kb + (size_t)n * a.Hkv * D + j * SL);
 #pragma unroll
       for (int i = 0; i < SL / 4; ++i) kv[i] = kr[i];
     }
   }
   const int c = t % TPR, rg = t / TPR;
-  const size_t base = (((size_t)b * bstride + row0 + r0) * Hq + h) * D + c * E;
+  const size_t base = (((size_t)b * a.q_bstride + a.q_row0 + r0) * Hq + h) * D + c * E;
   u32x4 w[IT];
 #pragma unroll
   for (int it = 0; it < IT; ++it) {
     const int r = rg + it * NG;
-    w[it] = r < nr ? *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(q_dec) +
+    w[it] = r < nr ? *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(a.q_dec) +
                                                       (base + (size_t)r * Hq * D) * (BF16 ? 2 : 4))
                    : u32x4{0u, 0u, 0u, 0u};
   }
@@ -269,7 +268,7 @@ __global__ __launch_bounds__(256) void qscore_kernel(const void* q_dec, const fl
     float sum = 0.f;
 #pragma unroll
     for (int g = 0; g < NG; ++g) sum += red[g * D + t];
-    qp[t] = sum * (1.0f / rows);
+    qp[t] = sum * (1.0f / a.q_rows);
   }
   __syncthreads();
   float q[SL];
@@ -278,7 +277,7 @@ __global__ __launch_bounds__(256) void qscore_kernel(const void* q_dec, const fl
   for (int n0 = 0; n0 < N; n0 += 32) {
     const int n = n0 + (t >> 3);
     if (n0 > 0 && n < N) {
-      const f32x4* kr = reinterpret_cast<const f32x4*>(kb + (size_t)n * Hkv * D + j * SL);
+      const f32x4* kr = reinterpret_cast<const f32x4*>(kb + (size_t)n * a.Hkv * D + j * SL);
 #pragma unroll
       for (int i = 0; i < SL / 4; ++i) kv[i] = kr[i];
     }
@@ -292,7 +291,80 @@ __global__ __launch_bounds__(256) void qscore_kernel(const void* q_dec, const fl
     acc2 += __shfl_xor(acc2, 1);
     acc2 += __shfl_xor(acc2, 2);
     acc2 += __shfl_xor(acc2, 4);
-    if (j == 0 && n < N) partial[((size_t)b * N + n) * Hq * NS + (size_t)h * NS + sp] = acc2 * scale;
+    if (j == 0 && n < N) a.partial[((size_t)b * N + n) * Hq * NS + (size_t)h * NS + sp] = acc2 * a.scale;
+  }
+}
+
+template <bool BF16, int D>
+__global__ __launch_bounds__(256) void qscore_kernel(SelectArgs a) {
+  qscore_terms<BF16, D>(a, blockIdx.x);
+}
+
+// Chunk scores of sequence b: the T terms of each chunk summed 8 lanes per
+// chunk (lane j sums terms j, j+8, ...), then a fixed xor butterfly over the 8
+// lanes; keys[n] = rank key of the score (negated when neg), keys past N =
+// max.  Writes chunk_score[b][n] when `out` is given.
+__device__ void chunk_keys(const float* partial, int b, int N, int T, int Npad, int neg, uint64_t* keys,
+                           float* out) {
+  const int t = threadIdx.x;
+  for (int n = t; n < Npad; n += 256) keys[n] = ~0ull;
+  __syncthreads();
+  const int j = t & 7;
+  for (int n0 = 0; n0 < N; n0 += 32) {
+    const int n = n0 + (t >> 3);
+    float s = 0.f;
+    if (n < N) {
+      const float* pr = partial + ((size_t)b * N + n) * T;
+#pragma unroll 16
+      for (int i = j; i < T; i += 8) s += pr[i];
+    }
+    s += __shfl_xor(s, 1);
+    s += __shfl_xor(s, 2);
+    s += __shfl_xor(s, 4);
+    if (j == 0 && n < N) {
+      keys[n] = rank_key(neg ? -s : s, n);
+      if (out) out[(size_t)b * N + n] = s;
+    }
+  }
+  __syncthreads();
+}
+
+// Kept tokens (rank < Bt) of one chunk in ascending order: counts over
+// contiguous segments, an exclusive scan (within each wave by shuffles, then
+// across the 4 waves), then each segment writes its slots (token + 1).  The
+// ranks of a segment are loaded 16 at a time, all in flight before the first
+// compare (a plain loop waits for each load in turn).
+__device__ void list_tokens(const int32_t* rk, int C, int Bt, int32_t* out, int* wsum) {
+  constexpr int U = 16;
+  const int t = threadIdx.x;
+  const int seg = (C + 255) / 256;
+  const int j0 = min(C, t * seg), j1 = min(C, j0 + seg);
+  int cnt = 0;
+  for (int base = j0; base < j1; base += U) {
+    int r[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) r[u] = base + u < j1 ? rk[base + u] : Bt;
+#pragma unroll
+    for (int u = 0; u < U; ++u) cnt += r[u] < Bt;
+  }
+  const int lane = t & 63, wv = t >> 6;
+  int inc = cnt;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(inc, o);
+    if (lane >= o) inc += y;
+  }
+  if (lane == 63) wsum[wv] = inc;
+  __syncthreads();
+  int pos = inc - cnt;
+  for (int w = 0; w < wv; ++w) pos += wsum[w];
+  for (int base = j0; base < j1; base += U) {
+    int r[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) r[u] = base + u < j1 ? rk[base + u] : Bt;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (r[u] < Bt) out[pos++] = base + u + 1;
   }
 }
 
@@ -303,39 +375,12 @@ __global__ __launch_bounds__(256) void select_kernel(const float* partial, const
                                                       float* chunk_score, int32_t* chunk_idx, int32_t* tok_slot,
                                                       int N, int C, int K, int Bt, int T, int Npad, int neg) {
   extern __shared__ __attribute__((aligned(16))) uint64_t keys[];
-  __shared__ int my_chunk;
   __shared__ int rankv[256];
   __shared__ int wsum[4];
+  __shared__ int my_chunk;
   const int b = blockIdx.x / K, k = blockIdx.x % K;
   const int t = threadIdx.x;
-
-  // Chunk scores: the T = Hq*NS terms of each chunk, 8 lanes per chunk (lane j
-  // sums terms j, j+8, ...), then a fixed xor butterfly over the 8 lanes.
-  for (int n = t; n < Npad; n += 256) keys[n] = ~0ull;
-  __syncthreads();
-  {
-    const int j = t & 7;
-    for (int n0 = 0; n0 < N; n0 += 32) {
-      const int n = n0 + (t >> 3);
-      float s = 0.f;
-      if (n < N) {
-        const float* pr = partial + ((size_t)b * N + n) * T;
-#pragma unroll 8
-        for (int i = j; i < T; i += 8) s += pr[i];
-      }
-      s += __shfl_xor(s, 1);
-      s += __shfl_xor(s, 2);
-      s += __shfl_xor(s, 4);
-      if (j == 0 && n < N) {
-        keys[n] = rank_key(neg ? -s : s, n);
-        if (k == 0 && chunk_score) chunk_score[(size_t)b * N + n] = s;
-      }
-    }
-  }
-  __syncthreads();
-  // The K kept chunks (the K smallest keys) in ascending index order.  Up to
-  // 256 chunks: each chunk's rank by counting the smaller keys (keys are
-  // distinct: the index is in the low bits); beyond, a bitonic sort.
+  chunk_keys(partial, b, N, T, Npad, neg, keys, k == 0 ? chunk_score : nullptr);
   if (N <= 256) {
     if (t < N) {
       const uint64_t me = keys[t];
@@ -361,36 +406,13 @@ __global__ __launch_bounds__(256) void select_kernel(const float* partial, const
     }
   }
   __syncthreads();
-  const int32_t* rk = tok_rank + ((size_t)b * N + my_chunk) * C;
-
-  // Kept tokens (rank < Bt) in ascending order: counts over contiguous segments,
-  // an exclusive scan (within each wave by shuffles, then across the 4 waves),
-  // then each segment writes its slots.
-  const int seg = (C + 255) / 256;
-  const int j0 = t * seg, j1 = min(C, j0 + seg);
-  int cnt = 0;
-  for (int j = j0; j < j1; ++j) cnt += rk[j] < Bt;
-  const int lane = t & 63, wv = t >> 6;
-  int inc = cnt;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(inc, o);
-    if (lane >= o) inc += y;
-  }
-  if (lane == 63) wsum[wv] = inc;
-  __syncthreads();
-  int pos = inc - cnt;
-  for (int w = 0; w < wv; ++w) pos += wsum[w];
-  int32_t* out = tok_slot + ((size_t)b * K + k) * Bt;
-  for (int j = j0; j < j1; ++j)
-    if (rk[j] < Bt) out[pos++] = j + 1;
+  list_tokens(tok_rank + ((size_t)b * N + my_chunk) * C, C, Bt, tok_slot + ((size_t)b * K + k) * Bt, wsum);
 }
 
 hipError_t launch_score_select(const SelectArgs& a, hipStream_t s) {
   const dim3 g1(a.B * a.Hq * a.NS);
-#define PD_QSCORE(BF, DD)                                                                                      \
-  hipLaunchKernelGGL((qscore_kernel<BF, DD>), g1, dim3(256), 0, s, a.q_dec, a.key_mean, a.partial, a.N, a.Hq, \
-                     a.Hkv, a.G, a.q_rows, a.q_row0, a.q_bstride, a.NS, a.scale)
+  const int Npad = next_pow2(a.N);
+#define PD_QSCORE(BF, DD) hipLaunchKernelGGL((qscore_kernel<BF, DD>), g1, dim3(256), 0, s, a)
   if (a.D == 128) {
     if (a.bf16) PD_QSCORE(true, 128); else PD_QSCORE(false, 128);
   } else {
@@ -399,7 +421,6 @@ hipError_t launch_score_select(const SelectArgs& a, hipStream_t s) {
 #undef PD_QSCORE
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  const int Npad = next_pow2(a.N);
   hipLaunchKernelGGL(select_kernel, dim3(a.B * a.K), dim3(256), (size_t)Npad * 8, s, a.partial, a.tok_rank,
                      a.chunk_score, a.chunk_idx, a.tok_slot, a.N, a.C, a.K, a.Bt, a.Hq * a.NS, Npad, 0);
   return hipGetLastError();

@@ -21,7 +21,8 @@ def torch_dtype(d: Dims):
 
 
 def workspace(nbytes, device="cuda"):
-    return torch.empty(max(nbytes, 16), dtype=torch.uint8, device=device)
+    """Caller-owned scratch (zero-filled, so that a stale value never passes for a result)."""
+    return torch.zeros(max(nbytes, 16), dtype=torch.uint8, device=device)
 
 
 def run_prefill(d: Dims, x, stream=None, chunk_score=False):

@@ -167,6 +167,7 @@ SELECT_CASES = [
     (PD_BF16, 1, 1, 33, 3, 2, 2, 64, 1, 1),
     (PD_FP32, 2, 40, 300, 9, 4, 4, 64, 7, 33),
     (PD_FP32, 1, 1024, 16, 4, 2, 1, 64, 10, 16),
+    (PD_BF16, 2, 100, 40, 20, 4, 2, 64, 80, 9),     # K > 64: the two-launch selection
 ]
 
 
@@ -187,6 +188,31 @@ def test_select_parity(case):
         check_topk_rule_a(s_ref[b], ci[b].cpu().numpy(), K)
     want = oracle.tokens_by_rank_ref(rank.cpu().numpy(), ci.cpu().numpy(), Bt)
     assert np.array_equal(tsl.cpu().numpy(), want)
+
+
+def test_select_repeated_calls_one_workspace():
+    """Calls in a row on one workspace (different batch sizes and K) each match the oracle: nothing a call
+    leaves in the workspace leaks into the next."""
+    from gpu_path import workspace
+    from paper_2606_10537_amd import _lib
+    g = torch.Generator().manual_seed(77)
+    big = Dims(6, 12, 64, 4, 0, 300, 8, 4, 64, PD_BF16)
+    ws = workspace(_lib.pd_workspace_bytes(big, 12, 64, 0, 1))
+    for it, (B, K) in enumerate([(6, 3), (2, 5), (6, 12), (4, 1), (6, 3)]):
+        d = Dims(B, 12, 64, 4, 0, 300, 8, 4, 64, PD_BF16)
+        q = torch.randn((B, 300, 8, 64), generator=g).to(torch.bfloat16).cuda()
+        km = torch.randn((B, 12, 4, 64), generator=g).cuda()
+        rank = torch.argsort(torch.rand((B, 12, 64), generator=g), dim=2).to(torch.int32).cuda()
+        ci = torch.full((B, K), -1, dtype=torch.int32, device="cuda")
+        ts = torch.full((B, K, 20), -1, dtype=torch.int32, device="cuda")
+        cs = torch.full((B, 12), float("nan"), dtype=torch.float32, device="cuda")
+        _lib.pd_score_select(d, K, 20, q, km, rank, ci, ts, cs, ws)
+        torch.cuda.synchronize()
+        s_ref = oracle.chunk_scores_ref(h64(q), h64(km))
+        np.testing.assert_allclose(h64(cs), s_ref, rtol=1e-5, atol=1e-5)
+        for b in range(B):
+            check_topk_rule_a(s_ref[b], ci[b].cpu().numpy(), K)
+        assert np.array_equal(ts.cpu().numpy(), oracle.tokens_by_rank_ref(rank.cpu().numpy(), ci.cpu().numpy(), 20))
 
 
 def test_prefill_then_select_end_to_end():
