@@ -162,6 +162,23 @@ pd_status pd_score_select(const pd_dims *dims, int32_t top_k, int32_t tok_budget
                           void *workspace, size_t ws_bytes, void *stream);
 
 /*
+ * pd_score_select without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, outputs and errors as
+ * pd_score_select minus the workspace: its scratch (the B*N*H_q*ceil(L_d/128)
+ * fp32 chunk-score terms, rounded up to 256 bytes) lives in a static array of
+ * 4 MiB per GPU, held by the library from the first call on that GPU until the
+ * process ends; a call that needs more returns PD_ERR_BAD_DIMS.  The current device's array is used (call
+ * with the stream's device current).  Every call on one GPU shares that
+ * array: calls that overlap in time on one GPU (other streams, other threads)
+ * race and must be serialised by the caller.  Nothing is allocated and nothing
+ * needs clearing: every call rewrites the terms before it reads them.
+ */
+pd_status pd_score_select_noalloc(const pd_dims *dims, int32_t top_k, int32_t tok_budget,
+                                  const void *q_dec, const float *key_mean, const int32_t *tok_rank,
+                                  int32_t *chunk_idx, int32_t *tok_slot, float *chunk_score, void *stream);
+
+/*
  * Stage (c), one layer, one denoising step: the L_d decode rows attend
  * (bidirectionally) over, in order, for each kept chunk chunk_idx[b][k]: its
  * BOS row (cache slot 0) and the rows at slots tok_slot[b][k][*]; then rows

@@ -21,7 +21,7 @@ EXPORTS = ["pd_prefill_chunks", "pd_score_select", "pd_sparse_decode_attn", "pd_
            "pd_workspace_bytes", "pd_decode_splits", "pd_status_string", "pd_last_error_message",
            "pd_version", "pd_mfma_rate_probe", "pd_score_select_static", "pd_gather_selected",
            "pd_sparse_decode_attn_compact", "pd_compact_workspace_bytes", "pd_select_ranked",
-           "pd_gather_joint"]
+           "pd_gather_joint", "pd_score_select_noalloc"]
 
 
 class PdError(RuntimeError):
@@ -104,6 +104,8 @@ def load(path: str = LIB_PATH):
     lib.pd_last_error_message.restype = ctypes.c_char_p
     lib.pd_select_ranked.argtypes = [dp, i32, i32, fp, i32, fp, vp, vp, vp]
     lib.pd_select_ranked.restype = ctypes.c_int
+    lib.pd_score_select_noalloc.argtypes = [dp, i32, i32, vp, fp, fp, vp, vp, fp, vp]
+    lib.pd_score_select_noalloc.restype = ctypes.c_int
     lib.pd_score_select_static.argtypes = [dp, i32, i32, vp, fp, fp, vp, vp, fp, vp, sz, vp]
     lib.pd_score_select_static.restype = ctypes.c_int
     lib.pd_gather_selected.argtypes = [dp, i32, i32] + [vp] * 6 + [vp]
@@ -185,6 +187,14 @@ def pd_score_select(dims: Dims, top_k, tok_budget, q_dec, key_mean, tok_rank, ch
         ctypes.byref(dims.c()), top_k, tok_budget, _ptr(q_dec), _ptr(key_mean), _ptr(tok_rank),
         _ptr(chunk_idx), _ptr(tok_slot), _ptr(chunk_score), _ptr(workspace), _nbytes(workspace),
         _stream(stream)))
+
+
+def pd_score_select_noalloc(dims: Dims, top_k, tok_budget, q_dec, key_mean, tok_rank, chunk_idx, tok_slot,
+                            chunk_score=None, stream=None):
+    """Stage (b) without a workspace: scratch in the library's static per-GPU array (see include/pd.h)."""
+    _check(load().pd_score_select_noalloc(
+        ctypes.byref(dims.c()), top_k, tok_budget, _ptr(q_dec), _ptr(key_mean), _ptr(tok_rank),
+        _ptr(chunk_idx), _ptr(tok_slot), _ptr(chunk_score), _stream(stream)))
 
 
 def pd_sparse_decode_attn(dims: Dims, top_k, tok_budget, q_dec, k_dec, v_dec, k_cache, v_cache,

@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "pd.h"
@@ -375,7 +376,37 @@ pd_status pd_select_ranked(const pd_dims* d, int32_t top_k, int32_t tok_budget, 
 
 }  // extern "C"
 
+// Scratch of pd_score_select_noalloc: one array per GPU holding the selection
+// workspace (the chunk-score terms, fully rewritten by every call before the
+// selection kernel reads them, so nothing needs clearing).  Host code never passes the array's name to a kernel:
+// the address of each device's copy comes from hipGetSymbolAddress.
+constexpr size_t kNoallocScratchBytes = 4u << 20;
+static __device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch[kMaxDevices];
+
+// Device address of the current device's scratch, looked up once per device.
+pd_status scratch_of_current_device(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(PD_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(PD_ERR_UNSUPPORTED, "device %d is beyond the %d devices of the scratch table", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(PD_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return PD_OK;
+}
 
 // Shared by the selection entry points: sizes and pointers checked here, the
 // mean query over `rows` rows starting at row0 of every bstride rows of q.
@@ -433,6 +464,23 @@ pd_status pd_score_select(const pd_dims* d, int32_t top_k, int32_t tok_budget, c
   PD_RETURN_IF(select_args(d, top_k, tok_budget, q_dec, key_mean, tok_rank, chunk_idx, tok_slot, chunk_score, &a));
   PD_RETURN_IF(check_ws(workspace, ws_bytes, select_ws(d)));
   place_select_ws(workspace, &a);
+  return hip_status(pd::launch_score_select(a, (hipStream_t)stream), "score/select kernels");
+}
+
+pd_status pd_score_select_noalloc(const pd_dims* d, int32_t top_k, int32_t tok_budget, const void* q_dec,
+                                  const float* key_mean, const int32_t* tok_rank, int32_t* chunk_idx,
+                                  int32_t* tok_slot, float* chunk_score, void* stream) {
+  PD_RETURN_IF(check_dims(d));
+  pd::SelectArgs a;
+  PD_RETURN_IF(select_args(d, top_k, tok_budget, q_dec, key_mean, tok_rank, chunk_idx, tok_slot, chunk_score, &a));
+  const size_t need = select_ws(d);
+  if (need > kNoallocScratchBytes)
+    return fail(PD_ERR_BAD_DIMS,
+                "selection needs %zu bytes of scratch (B*N*H_q*ceil(L_d/128)*4); the static scratch holds %zu",
+                need, kNoallocScratchBytes);
+  void* ws = nullptr;
+  PD_RETURN_IF(scratch_of_current_device(&ws));
+  place_select_ws(ws, &a);
   return hip_status(pd::launch_score_select(a, (hipStream_t)stream), "score/select kernels");
 }
 

@@ -121,6 +121,26 @@ def test_decode_validation(lib):
     assert call(splits=4, w=None) == 5
 
 
+def test_noalloc_select_validation(lib):
+    """The scratch-array selection checks its arguments and rejects sizes beyond its 4 MiB array on the
+    host, before it looks up the device array (so none of these calls touches the HIP runtime)."""
+    d = dims()
+    c = ctypes.byref(d.c())
+    call = lambda k=2, bt=64, q=A, ci=A, cs=None, dd=c: lib.pd_score_select_noalloc(dd, k, bt, q, A, A, ci, A, cs,
+                                                                                    None)
+    assert call(dd=None) == 1
+    assert call(k=0) == 2
+    assert call(k=5) == 2
+    assert call(bt=129) == 2
+    assert call(q=None) == 1
+    assert call(ci=MIS) == 4
+    assert call(cs=MIS) == 4
+    big = dims(batch=64, n_chunks=1024, chunk_len=64, n_heads_q=64, n_heads_kv=8, dec_len=512)
+    assert 64 * 1024 * 64 * 4 * 4 > 4 << 20
+    assert call(dd=ctypes.byref(big.c())) == 2
+    assert b"scratch" in lib.pd_last_error_message()
+
+
 def test_static_mode_validation(lib):
     d = dims()
     c = ctypes.byref(d.c())
