@@ -36,6 +36,11 @@ def parse():
     p.add_argument("--dec-pool", type=int, default=4, help="decode input slots per layer")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU time budget of the oracle sample")
+    p.add_argument("--cpu-mode", choices=("auto", "sample", "full"), default="auto",
+                   help="oracle timing: every unit of one job step (full; the default for workloads 1-3) or a "
+                        "bounded sample extrapolated to one step (sample; the default for workloads 4-5)")
+    p.add_argument("--no-workloads", action="store_true",
+                   help="skip the measurements of workloads 2-4 after the timed region")
     p.add_argument("--flush-mib", type=int, default=0,
                    help="write this many MiB before every decode launch, so that each launch starts with the "
                         "last-level cache (MALL) holding none of its operands (cold numbers)")
@@ -80,7 +85,7 @@ def algorithmic(w, layers):
     """Algorithmic FLOPs / bytes per launch of the prefill and decode attention kernels."""
     B, N, C, Lq, Lm, Ld = w.batch, w.n_chunks, w.chunk_len, w.q_len, w.m_len, w.dec_len
     Hq, Hkv, d, K, Bt = w.n_heads_q, w.n_heads_kv, w.head_dim, w.top_k, w.tok_budget
-    eb = 2
+    eb = 2 if w.dtype == 0 else 4   # bytes per element: bf16 (PD_BF16 = 0) or fp32
     Sc = 1 + C + Lq + Lm
     L_kv = K * (1 + Bt) + Lq + Ld
     pre_flop = 4.0 * Sc * Sc * d * Hq * B * N
@@ -93,54 +98,175 @@ def algorithmic(w, layers):
     return pre_flop, pre_bytes, dec_flop, dec_bytes
 
 
-def cpu_baseline(w, budget_s):
-    """Time the fp64 oracle on a bounded sample of the same workload, extrapolated to one step."""
+# ---- CPU baseline: the fp64 oracle on the host cores ---------------------------------------------
+# A process pool over independent units, one BLAS thread per worker: prefill units (sequence, chunk,
+# query head), selection units (step, sequence) and decode units (step, sequence, query head).  Workers
+# draw the workload's inputs themselves (the same seeded generator the GPU run uses) and never touch
+# the GPU.  Workloads 1-3 are timed in full (every unit of one job step); workloads 4-5 are timed on a
+# bounded sample of each unit kind with every worker busy, and the step time is extrapolated from the
+# measured pool throughput and the unit counts.
+CPU_SHARE = 16   # host cores one GPU's share of the box provides
+
+
+def _cpu_host_info(workers):
+    import platform
     import numpy as np
     from threadpoolctl import threadpool_info
+    model = platform.processor() or ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), model)
+    except OSError:
+        pass
+    blas = [f"{i.get('internal_api')} {i.get('version')}" for i in threadpool_info() if i.get("user_api") == "blas"]
+    return {"cores": workers, "affinity_cpus": len(os.sched_getaffinity(0)), "os_cpu_count": os.cpu_count(),
+            "cpu_model": model, "numpy": np.__version__, "blas": ", ".join(blas) or "none found",
+            "blas_threads_per_worker": 1}
 
-    import oracle
+
+_CW = {}   # per-worker state: workload, its prefill inputs (fp32 copies of the exact values), decode cache
+
+
+def _cpu_worker_init(wid, full):
+    from threadpoolctl import threadpool_limits
+    threadpool_limits(1)
     from paper_2606_10537_amd import synth
+    w = synth.WORKLOADS[wid]
+    if not full:   # one sequence, one chunk of the workload's shapes
+        w = synth.Workload(**{**w.__dict__, "batch": 1, "n_chunks": 1})
+    x = synth.make_prefill(w, 0, "cpu")
+    _CW.update(w=w, x={k: v.float().numpy() for k, v in x.items()}, dec_t=None)
 
-    rng = np.random.default_rng(0)
-    B, N, C, Lq, Lm, Ld = w.batch, w.n_chunks, w.chunk_len, w.q_len, w.m_len, w.dec_len
-    Hq, Hkv, d, K, Bt = w.n_heads_q, w.n_heads_kv, w.head_dim, w.top_k, w.tok_budget
+
+def _cpu_decode_inputs(t):
+    from paper_2606_10537_amd import synth
+    if _CW["dec_t"] != t:
+        d = synth.make_decode(_CW["w"], 0, t, "cpu")
+        _CW.update(dec={k: v.float().numpy() for k, v in d.items()}, dec_t=t)
+    return _CW["dec"]
+
+
+def _cpu_prefill_unit(b, n, h):
+    """One prefill unit; returns (seconds, this head's Eq. 5 term, b, n)."""
+    import oracle
+    x, w = _CW["x"], _CW["w"]
+    t0 = time.perf_counter()
+    u = oracle.prefill_unit_ref(x["q_pre"], x["k_pre"], x["v_pre"], x["q_qm"], x["k_qm"], x["v_qm"], b, n, h,
+                                w.q_len)
+    return time.perf_counter() - t0, u["e_head"], b, n
+
+
+def _cpu_select_unit(t, key_mean, tok_score):
+    """Selection of step t for every sequence; returns (seconds, chunk_idx, tok_slot)."""
+    import oracle
+    w = _CW["w"]
+    q = _cpu_decode_inputs(t)["q_dec"]
+    t0 = time.perf_counter()
+    ci, ts, _ = oracle.score_select_ref(q, key_mean, tok_score, w.top_k, w.tok_budget)
+    return time.perf_counter() - t0, ci, ts
+
+
+def _cpu_decode_unit(t, b, h, chunk_idx, tok_slot):
+    """One decode unit (step t, sequence b, query head h) over the chunk cache, a transposed view of the
+    worker's prefill inputs; chunk_idx (B, K) and tok_slot (B, K, B_tok) as the selection wrote them.
+    Returns seconds."""
+    import numpy as np
+    import oracle
+    x, w = _CW["x"], _CW["w"]
+    dec = _cpu_decode_inputs(t)
+    kc = np.transpose(x["k_pre"], (0, 1, 3, 2, 4))
+    vc = np.transpose(x["v_pre"], (0, 1, 3, 2, 4))
+    t0 = time.perf_counter()
+    oracle.decode_unit_ref(dec["q_dec"], dec["k_dec"], dec["v_dec"], kc, vc, chunk_idx, tok_slot, x["k_qm"],
+                           x["v_qm"], w.q_len, b, h)
+    return time.perf_counter() - t0
+
+
+def _cpu_decode_unit_sample(t, h):
+    """A decode unit of the sample mode: the K kept chunks are K copies of the one chunk, the kept slots
+    the first B_tok (the work does not depend on which rows are kept)."""
+    import numpy as np
+    w = _CW["w"]
+    ci = np.zeros((1, w.top_k), dtype=np.int32)
+    ts = np.tile(np.arange(1, w.tok_budget + 1, dtype=np.int32), (1, w.top_k, 1))
+    return _cpu_decode_unit(t, 0, h, ci, ts)
+
+
+def _cpu_select_unit_sample(t):
+    import numpy as np
+    w = _CW["w"]
+    rng = np.random.default_rng(t)
+    km = rng.standard_normal((1, max(w.top_k, 1), w.n_heads_kv, w.head_dim))
+    ts = rng.standard_normal((1, km.shape[1], w.chunk_len))
+    return _cpu_select_unit(t, km, ts)[0]
+
+
+def cpu_baseline(w, budget_s, mode):
+    """The fp64 oracle, timed on the host cores (see the section comment); returns the cpu_baseline
+    object of the JSON line."""
+    import concurrent.futures as cf
+    import multiprocessing as mp
+    import numpy as np
+    workers = max(1, min(len(os.sched_getaffinity(0)), CPU_SHARE))
+    for var in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS"):
+        os.environ[var] = "1"   # inherited by the spawned workers before they import numpy
+    full = mode == "full" or (mode == "auto" and w.cid <= 3)
+    B, N, C, Hq, Hkv, d, K = w.batch, w.n_chunks, w.chunk_len, w.n_heads_q, w.n_heads_kv, w.head_dim, w.top_k
     L, T = w.layers, w.steps
-    # One sequence, one chunk of the workload's shapes (values from the synthetic generator).
-    w1 = synth.Workload(**{**w.__dict__, "batch": 1, "n_chunks": 1})
-    x = {k: v.double().numpy() for k, v in synth.make_prefill(w1, 0, "cpu").items()}
-    dec = {k: v.double().numpy() for k, v in synth.make_decode(w1, 0, 0, "cpu").items()}
+    info = _cpu_host_info(workers)
+    ctx = mp.get_context("spawn")
+    with cf.ProcessPoolExecutor(workers, mp_context=ctx, initializer=_cpu_worker_init,
+                                initargs=(w.cid, full)) as ex:
+        list(ex.map(time.sleep, [0.01] * workers))   # all workers up (imports, inputs) before timing
+        if full:
+            from paper_2606_10537_amd import synth
+            x = {k: v.float().numpy() for k, v in synth.make_prefill(w, 0, "cpu").items()}
+            t0 = time.perf_counter()
+            futs = [ex.submit(_cpu_prefill_unit, b, n, h) for b in range(B) for n in range(N) for h in range(Hq)]
+            e = np.zeros((B, N, C))
+            for f in futs:
+                _, eh, b, n = f.result()
+                e[b, n] += eh
+            import oracle
+            km = oracle.key_mean_ref(x["k_pre"])
+            t_pre = time.perf_counter() - t0
+            for t in range(T):
+                _, ci, ts = ex.submit(_cpu_select_unit, t, km, e).result()
+                dfuts = [ex.submit(_cpu_decode_unit, t, b, h, ci, ts) for b in range(B) for h in range(Hq)]
+                for f in dfuts:
+                    f.result()
+            step_s = (time.perf_counter() - t0) * L
+            return {"value": T / step_s, "unit": "denoising steps/s", "kind": "oracle", "mode": "full",
+                    "seconds_per_step": step_s, "prefill_s": t_pre * L, **info,
+                    "sample": (f"fp64 oracle, every unit of one job step: {B * N * Hq * L} prefill units "
+                               f"(S_c={1 + C + w.q_len + w.m_len}), {T * L} selections, {B * Hq * T * L} decode "
+                               f"units (L_kv={K * (1 + w.tok_budget) + w.q_len + w.dec_len}), {workers} worker "
+                               f"processes, 1 BLAS thread each")}
 
-    def timed(fn, share):
-        n, t0 = 0, time.perf_counter()
-        while True:
-            fn()
-            n += 1
-            el = time.perf_counter() - t0
-            if el >= share * budget_s:
-                return el / n, n
+        def pool_rate(fn, args_list, share):
+            """Units per second with every worker busy, on rounds of `workers` units within the budget."""
+            n, t0 = 0, time.perf_counter()
+            while True:
+                list(ex.map(fn, *zip(*args_list)))
+                n += len(args_list)
+                if time.perf_counter() - t0 >= share * budget_s:
+                    return n / (time.perf_counter() - t0), n
 
-    t_pre, n_pre = timed(lambda: oracle.prefill_unit_ref(x["q_pre"], x["k_pre"], x["v_pre"], x["q_qm"], x["k_qm"],
-                                                         x["v_qm"], 0, 0, 0, Lq), 0.5)
-    km = rng.standard_normal((1, N, Hkv, d))
-    ts = rng.standard_normal((1, N, C))
-    qd = rng.standard_normal((1, Ld, Hq, d))
-    t_sel, n_sel = timed(lambda: oracle.score_select_ref(qd, km, ts, K, Bt), 0.15)
-    kc = rng.standard_normal((1, K, Hkv, 1 + C, d))
-    vc = rng.standard_normal((1, K, Hkv, 1 + C, d))
-    ci = np.arange(K, dtype=np.int32)[None]
-    tsl = np.sort(rng.permuted(np.tile(np.arange(1, C + 1), (1, K, 1)), axis=2)[:, :, :Bt], axis=2).astype(np.int32)
-    t_dec, n_dec = timed(lambda: oracle.decode_unit_ref(dec["q_dec"], dec["k_dec"], dec["v_dec"], kc, vc, ci, tsl,
-                                                        x["k_qm"], x["v_qm"], Lq, 0, 0), 0.35)
-    step_s = t_pre * B * N * Hq * L + t_sel * B * T * L + t_dec * B * Hq * T * L
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    return {
-        "value": T / step_s, "unit": "denoising steps/s", "cores": threads, "kind": "oracle",
-        "sample": (f"fp64 oracle: {n_pre} prefill units (1 chunk x 1 head, S_c={1 + C + Lq + Lm}), "
-                   f"{n_sel} score/select calls (1 sequence), {n_dec} decode units (1 sequence x 1 head, "
-                   f"L_kv={K * (1 + Bt) + Lq + Ld}); per-unit times x unit counts of one step "
-                   f"({B * N * Hq * L} prefill, {B * T * L} select, {B * Hq * T * L} decode units); extrapolated"),
-        "seconds_per_step_extrapolated": step_s,
-    }
+        r_pre, n_pre = pool_rate(_cpu_prefill_unit, [(0, 0, h % Hq) for h in range(workers)], 0.5)
+        r_sel, n_sel = pool_rate(_cpu_select_unit_sample, [(t,) for t in range(workers)], 0.1)
+        r_dec, n_dec = pool_rate(_cpu_decode_unit_sample, [(t % 4, h % Hq) for t, h in
+                                                           zip(range(workers), range(workers))], 0.4)
+    # one selection unit of the sample covers one sequence: B of them per (step, layer)
+    units_pre, units_sel, units_dec = B * N * Hq * L, B * T * L, B * Hq * T * L
+    step_s = units_pre / r_pre + units_sel / r_sel + units_dec / r_dec
+    return {"value": T / step_s, "unit": "denoising steps/s", "kind": "oracle", "mode": "extrapolated",
+            "seconds_per_step_extrapolated": step_s,
+            "pool_units_per_s": {"prefill": r_pre, "select": r_sel, "decode": r_dec}, **info,
+            "sample": (f"fp64 oracle on {workers} worker processes (1 BLAS thread each): {n_pre} prefill units "
+                       f"(1 chunk x 1 head, S_c={1 + C + w.q_len + w.m_len}), {n_sel} selections (1 sequence), "
+                       f"{n_dec} decode units (1 sequence x 1 head, L_kv={K * (1 + w.tok_budget) + w.q_len + w.dec_len}); "
+                       f"pool throughput x unit counts of one job step ({units_pre} prefill, {units_sel} "
+                       f"selection, {units_dec} decode units); extrapolated")}
 
 
 def static_mode(torch, _lib, w, d, pool, dec_pool, k_cache, v_cache, key_mean, tok_rank, stream, dec_flop,
@@ -369,20 +495,12 @@ def achievable_peaks(torch, dev):
                       "and a 4 GiB device copy (read + write bytes)"}
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (got --gpus {args.gpus}); the path shards by "
-              "sequence with no communication, so multi-GPU figures are not produced.", file=sys.stderr)
-        sys.exit(2)
-    import torch
-
-    from paper_2606_10537_amd import _lib, synth
-
-    lib = _lib.load()
-    w = synth.WORKLOADS[args.workload]
-    if args.layers:
-        w = synth.Workload(**{**w.__dict__, "layers": args.layers})
+def measure(torch, _lib, w, steps, warmup, pool_n=2, dec_pool_n=4, flush_mib=0, calib_copy_mib=0, log=""):
+    """Inputs resident in HBM, then `warmup` untimed and `steps` timed job steps of workload w: prefill of
+    every layer, then T denoising steps of (selection, sparse decode) for every layer.  HIP events on the
+    launch stream around every prefill, selection and decode launch.  Returns the timings and the
+    resident buffers (the select-once schedules reuse them)."""
+    from paper_2606_10537_amd import synth
     d = w.dims()
     dev = "cuda"
     dt = w.torch_dtype
@@ -390,9 +508,8 @@ def main():
     L, T, K, Bt, Ld = w.layers, w.steps, w.top_k, w.tok_budget, w.dec_len
     n_static = w.q_len
 
-    # ---- resident inputs and buffers -------------------------------------------------
-    pool = [synth.make_prefill(w, layer=i, device=dev) for i in range(min(args.pool, L))]
-    dec_slots = max(1, args.dec_pool)
+    pool = [synth.make_prefill(w, layer=i, device=dev) for i in range(min(pool_n, L))]
+    dec_slots = max(1, dec_pool_n)
     dec_pool = [[synth.make_decode(w, layer=l, step=s, device=dev) for s in range(dec_slots)] for l in range(L)]
     o_pre = torch.empty((B, N, d.seq_len, Hq, D), dtype=dt, device=dev)
     k_cache = [torch.empty((B, N, Hkv, C + 1, D), dtype=dt, device=dev) for _ in range(L)]
@@ -410,11 +527,11 @@ def main():
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
 
-    flush = torch.empty(args.flush_mib << 20, dtype=torch.uint8, device=dev) if args.flush_mib else None
-    n_ev = L * T
-    ev_pre = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(L)]
-    ev_dec = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_ev)]
-    ev_mid = torch.cuda.Event(enable_timing=True)
+    flush = torch.empty(flush_mib << 20, dtype=torch.uint8, device=dev) if flush_mib else None
+    E = lambda: torch.cuda.Event(enable_timing=True)
+    ev_pre = [(E(), E()) for _ in range(L)]
+    ev_dec = [(E(), E()) for _ in range(L * T)]
+    ev_mid = E()
 
     def one_step(record):
         for l in range(L):
@@ -444,21 +561,21 @@ def main():
                     ev_dec[i][1].record(stream)
                 i += 1
 
-    if args.calib_copy_mib:
-        src = torch.empty(args.calib_copy_mib << 20, dtype=torch.uint8, device=dev)
+    if calib_copy_mib:
+        src = torch.empty(calib_copy_mib << 20, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         one_step(False)
     torch.cuda.synchronize()
 
-    pre_ms, dec_ms, dec_kernel_ms, step_ms = [], [], [], []
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    pre_ms, dec_ms, dec_kernel_ms, sel_ms, step_ms = [], [], [], [], []
+    start, end = E(), E()
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
-    for s in range(args.steps):
+    for s in range(steps):
         start.record(stream)
         one_step(True)
         end.record(stream)
@@ -467,83 +584,164 @@ def main():
         pre_ms.append(start.elapsed_time(ev_mid))
         dec_ms.append(ev_mid.elapsed_time(end))
         dec_kernel_ms.extend(a.elapsed_time(b) for a, b in ev_dec)
-        print(f"[bench] step {s}: {step_ms[-1]:.1f} ms (prefill {pre_ms[-1]:.1f} ms, decode loop {dec_ms[-1]:.1f} ms)",
-              file=sys.stderr, flush=True)
+        # between two decode launches: the next selection's launches and the gaps around them
+        sel_ms.extend(ev_dec[i - 1][1].elapsed_time(ev_dec[i][0]) for i in range(1, len(ev_dec)))
+        print(f"[bench]{log} step {s}: {step_ms[-1]:.1f} ms (prefill {pre_ms[-1]:.1f} ms, decode loop "
+              f"{dec_ms[-1]:.1f} ms)", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall
+    return {"d": d, "ms": sum(step_ms) / len(step_ms), "pre_ms_layer": sum(pre_ms) / len(pre_ms) / L,
+            "dec_loop_ms": sum(dec_ms) / len(dec_ms), "dec_kern_ms": sum(dec_kernel_ms) / len(dec_kernel_ms),
+            "sel_ms": sum(sel_ms) / len(sel_ms) if sel_ms else 0.0, "splits": splits, "wall": wall,
+            "bufs": {"pool": pool, "dec_pool": dec_pool, "o_pre": o_pre, "k_cache": k_cache, "v_cache": v_cache,
+                     "tok_score": tok_score, "tok_rank": tok_rank, "key_mean": key_mean, "ws_pre": ws_pre,
+                     "stream": stream}}
 
-    ms = sum(step_ms) / len(step_ms)
+
+def rates(w, m):
+    """Throughput and roofline figures of one measure() result."""
+    bf16 = w.dtype == 0
+    L, T = w.layers, w.steps
     pre_flop, pre_bytes, dec_flop, dec_bytes = algorithmic(w, L)
-    pre_ms_layer = sum(pre_ms) / len(pre_ms) / L
-    dec_kern_ms = sum(dec_kernel_ms) / len(dec_kernel_ms)
-    dec_tflops = dec_flop / (dec_kern_ms * 1e-3) / 1e12
-    dec_gbps = dec_bytes / (dec_kern_ms * 1e-3) / 1e9
-    pre_tflops = pre_flop / (pre_ms_layer * 1e-3) / 1e12
-    bf16 = w.dtype == _lib.PD_BF16
     peak_c = PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS
+    dk = m["dec_kern_ms"] * 1e-3
+    dec_tflops, dec_gbps = dec_flop / dk / 1e12, dec_bytes / dk / 1e9
     ridge = peak_c * 1e12 / (PEAK_HBM_GBPS * 1e9)
-    dec_bound = ("mfma" if bf16 else "alu") if dec_flop / dec_bytes > ridge else "hbm"
-    if dec_bound != "hbm":
-        roof = {"bound": dec_bound, "achieved": round(dec_tflops, 2), "peak": peak_c, "unit": "TFLOP/s",
-                "frac": round(dec_tflops / peak_c, 4)}
+    bound = ("mfma" if bf16 else "alu") if dec_flop / dec_bytes > ridge else "hbm"
+    binding = max(dec_flop / (peak_c * 1e12), dec_bytes / (PEAK_HBM_GBPS * 1e9)) / dk
+    pre_tflops = pre_flop / (m["pre_ms_layer"] * 1e-3) / 1e12
+    return {"dec_flop": dec_flop, "dec_bytes": dec_bytes, "dec_tflops": dec_tflops, "dec_gbps": dec_gbps,
+            "peak_c": peak_c, "bound": bound, "binding_frac": binding, "pre_tflops": pre_tflops,
+            "job_steps_per_s": T / (m["ms"] * 1e-3), "decode_steps_per_s": T / (m["dec_loop_ms"] * 1e-3)}
+
+
+def workload_summary(w, m):
+    """The per-workload object of the JSON line."""
+    r = rates(w, m)
+    unit = "GB/s" if r["bound"] == "hbm" else "TFLOP/s"
+    achieved = r["dec_gbps"] if r["bound"] == "hbm" else r["dec_tflops"]
+    peak = PEAK_HBM_GBPS if r["bound"] == "hbm" else r["peak_c"]
+    ctx = f"{w.context // 1024}K" if w.context >= 1024 else f"{w.context}-token"
+    return {"workload": f"{ctx} context ({w.name}): B={w.batch}, layers={w.layers}, N={w.n_chunks}, "
+                        f"C={w.chunk_len}, L_q={w.q_len}, L_m={w.m_len}, L_d={w.dec_len}, "
+                        f"H_q/H_kv={w.n_heads_q}/{w.n_heads_kv}, d={w.head_dim}, K={w.top_k}, "
+                        f"B_tok={w.tok_budget}, T={w.steps}",
+            "job_steps_per_s": round(r["job_steps_per_s"], 3), "ms_per_step": round(m["ms"], 4),
+            "decode_steps_per_s": round(r["decode_steps_per_s"], 3),
+            "decode_us_per_launch": round(m["dec_kern_ms"] * 1e3, 2),
+            "select_and_gaps_us_per_step": round(m["sel_ms"] * 1e3, 2),
+            "decode_splits": m["splits"],
+            "decode_roofline": {"bound": r["bound"], "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+                                "frac": round(achieved / peak, 4)},
+            "decode_tflops": round(r["dec_tflops"], 2), "decode_algorithmic_gbps": round(r["dec_gbps"], 1),
+            "decode_binding_roof_frac": round(r["binding_frac"], 4),
+            "prefill_ms_per_layer": round(m["pre_ms_layer"], 4), "prefill_tflops": round(r["pre_tflops"], 2),
+            "prefill_mfma_frac": round(r["pre_tflops"] / r["peak_c"], 4)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (got --gpus {args.gpus}); the path shards by "
+              "sequence with no communication, so multi-GPU figures are not produced.", file=sys.stderr)
+        sys.exit(2)
+    from paper_2606_10537_amd import synth
+    w = synth.WORKLOADS[args.workload]
+    if args.layers:
+        w = synth.Workload(**{**w.__dict__, "layers": args.layers})
+    cpu = None
+    if not args.no_cpu_baseline:
+        # Before any GPU work: the oracle's worker processes start from a process that has not
+        # initialised the GPU, and nothing else runs on the host meanwhile.
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w, args.cpu_seconds, args.cpu_mode)
+    import torch
+
+    from paper_2606_10537_amd import _lib
+    _lib.load()
+    m = measure(torch, _lib, w, args.steps, args.warmup, args.pool, args.dec_pool, args.flush_mib,
+                args.calib_copy_mib)
+    d = m["d"]
+    r = rates(w, m)
+    bf16 = w.dtype == _lib.PD_BF16
+    B, T, L, D = w.batch, w.steps, w.layers, w.head_dim
+    if r["bound"] != "hbm":
+        roof = {"bound": r["bound"], "achieved": round(r["dec_tflops"], 2), "peak": r["peak_c"], "unit": "TFLOP/s",
+                "frac": round(r["dec_tflops"] / r["peak_c"], 4)}
     else:
-        roof = {"bound": "hbm", "achieved": round(dec_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                "frac": round(dec_gbps / PEAK_HBM_GBPS, 4)}
+        roof = {"bound": "hbm", "achieved": round(r["dec_gbps"], 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                "frac": round(r["dec_gbps"] / PEAK_HBM_GBPS, 4)}
     kname = f"decode_{'bf16' if bf16 else 'f32'}_kernel<{D}>"
     roof.update({"kernel": f"{kname} (pd_sparse_decode_attn, one launch per layer and step)",
                  "traffic": measured_traffic() if (args.workload == 5 and not args.layers) else None,
-                 "launch_ms": round(dec_kern_ms, 5), "flop_per_launch": dec_flop,
-                 "bytes_per_launch": dec_bytes})
-
+                 "launch_ms": round(m["dec_kern_ms"], 5), "flop_per_launch": r["dec_flop"],
+                 "bytes_per_launch": r["dec_bytes"]})
     traffic = roof.get("traffic")
-    ctx = f"{w.context // 1024}K" if w.context >= 1024 else f"{w.context}-token"
+    summ = workload_summary(w, m)
     res = {
         "metric": "denoising steps/sec + decode-attn HBM GB/s + prefill MFMA TFLOP/s at 32K",
-        "value": round(T / (ms * 1e-3), 3),
+        "value": round(r["job_steps_per_s"], 3),
         "unit": "denoising steps/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms, 3),
+        "ms_per_step": round(m["ms"], 3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if bf16 else "f32", "data": "synthetic",
-        "config": {"workload": f"{ctx} context ({w.name}): B={B}, layers={L}, N={N}, C={C}, "
-                               f"L_q={w.q_len}, L_m={w.m_len}, L_d={Ld}, H_q/H_kv={Hq}/{Hkv}, d={D}, K={K}, "
-                               f"B_tok={Bt}, T={T}",
-                   "global_batch": B, "seq_len": w.context, "parallelism": "single GPU",
-                   "decode_splits": splits},
-        "decode_steps_per_s": round(T / (sum(dec_ms) / len(dec_ms) * 1e-3), 3),
-        "decode_attn_hbm_gbps": round(dec_gbps, 1),
-        "decode_attn_hbm_frac": round(dec_gbps / PEAK_HBM_GBPS, 4),
-        "decode_attn_tflops": round(dec_tflops, 2),
-        "prefill_ms_per_layer": round(pre_ms_layer, 3),
-        "prefill_tflops": round(pre_tflops, 2),
-        "prefill_mfma_frac": round(pre_tflops / peak_c, 4),
-        "compute_peak_tflops": peak_c,
-        "decode_dram_gbps": round(traffic / (dec_kern_ms * 1e-3) / 1e9, 1) if traffic else None,
-        "decode_binding_roof_frac": round(max(dec_flop / (peak_c * 1e12), dec_bytes / (PEAK_HBM_GBPS * 1e9))
-                                          / (dec_kern_ms * 1e-3), 4),
+        "config": {"workload": summ["workload"], "global_batch": B, "seq_len": w.context,
+                   "parallelism": "single GPU", "decode_splits": m["splits"]},
+        "decode_steps_per_s": round(r["decode_steps_per_s"], 3),
+        "decode_attn_hbm_gbps": round(r["dec_gbps"], 1),
+        "decode_attn_hbm_frac": round(r["dec_gbps"] / PEAK_HBM_GBPS, 4),
+        "decode_attn_tflops": round(r["dec_tflops"], 2),
+        "select_and_gaps_us_per_step": summ["select_and_gaps_us_per_step"],
+        "prefill_ms_per_layer": round(m["pre_ms_layer"], 3),
+        "prefill_tflops": round(r["pre_tflops"], 2),
+        "prefill_mfma_frac": round(r["pre_tflops"] / r["peak_c"], 4),
+        "compute_peak_tflops": r["peak_c"],
+        "decode_dram_gbps": round(traffic / (m["dec_kern_ms"] * 1e-3) / 1e9, 1) if traffic else None,
+        "decode_binding_roof_frac": round(r["binding_frac"], 4),
         "cold_flush_mib": args.flush_mib,
         "roofline": roof,
-        "wall_s": round(wall, 3),
+        "wall_s": round(m["wall"], 3),
     }
+    bufs = m.pop("bufs")
     if not args.no_static:
-        res["static_mode"] = static_mode(torch, _lib, w, d, pool, dec_pool, k_cache, v_cache, key_mean, tok_rank,
-                                         stream, dec_flop, pre_ms_layer, n_static)
-        res["prefill_score_mode"] = prefill_score_mode(torch, _lib, w, d, pool, (o_pre, tok_score, ws_pre),
-                                                       k_cache, v_cache, tok_rank, key_mean, stream,
-                                                       res["static_mode"]["loop_ms"])
-        res["full_mask_mode"] = full_mask_mode(torch, _lib, w, d, pool, dec_pool, (o_pre, tok_score, ws_pre),
-                                               k_cache, v_cache, tok_rank, key_mean, stream)
+        stream = bufs["stream"]
+        res["static_mode"] = static_mode(torch, _lib, w, d, bufs["pool"], bufs["dec_pool"], bufs["k_cache"],
+                                         bufs["v_cache"], bufs["key_mean"], bufs["tok_rank"], stream, r["dec_flop"],
+                                         m["pre_ms_layer"], w.q_len)
+        prefill_bufs = (bufs["o_pre"], bufs["tok_score"], bufs["ws_pre"])
+        res["prefill_score_mode"] = prefill_score_mode(torch, _lib, w, d, bufs["pool"], prefill_bufs,
+                                                       bufs["k_cache"], bufs["v_cache"], bufs["tok_rank"],
+                                                       bufs["key_mean"], stream, res["static_mode"]["loop_ms"])
+        res["full_mask_mode"] = full_mask_mode(torch, _lib, w, d, bufs["pool"], bufs["dec_pool"], prefill_bufs,
+                                               bufs["k_cache"], bufs["v_cache"], bufs["tok_rank"], bufs["key_mean"],
+                                               stream)
+    del bufs
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
     if not args.no_achievable:
-        ach = achievable_peaks(torch, dev)
+        ach = achievable_peaks(torch, "cuda")
         res["achievable"] = ach
         if roof["bound"] != "alu":   # the achievable rates are bf16 MFMA and HBM
             roof["frac_of_achievable"] = round(roof["achieved"] / (ach["mfma_tflops"] if roof["bound"] == "mfma"
                                                                    else ach["hbm_gbps"]), 4)
         if bf16:
-            res["prefill_frac_of_achievable"] = round(pre_tflops / ach["mfma_tflops"], 4)
-    if not args.no_cpu_baseline:
-        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
-        res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+            res["prefill_frac_of_achievable"] = round(r["pre_tflops"] / ach["mfma_tflops"], 4)
+    if not args.no_workloads:
+        # The other GPU workloads of the method's configurations, one after another after the timed
+        # region (each with its own resident inputs).
+        res["workloads"] = {}
+        for wid in (2, 3, 4):
+            if wid == args.workload:
+                continue
+            wk = synth.WORKLOADS[wid]
+            mk = measure(torch, _lib, wk, steps=3, warmup=1, log=f" workload {wid}")
+            mk.pop("bufs")
+            res["workloads"][str(wid)] = workload_summary(wk, mk)
+            torch.cuda.synchronize()
+            torch.cuda.empty_cache()
+    if cpu is not None:
+        res["cpu_baseline"] = cpu
     print(json.dumps(res))
 
 

@@ -28,8 +28,8 @@ def test_bench_refuses_several_gpus():
 @pytest.mark.gpu
 def test_bench_json_line():
     print("[bench contract] workload 2, 1 step, no warmup", flush=True)
-    r = run_bench("--workload", "2", "--steps", "1", "--warmup", "0", "--cpu-seconds", "1", "--no-static",
-                  "--no-achievable")
+    r = run_bench("--workload", "2", "--steps", "1", "--warmup", "0", "--cpu-seconds", "1", "--cpu-mode", "sample",
+                  "--no-static", "--no-achievable", "--no-workloads")
     assert r.returncode == 0, r.stderr[-2000:]
     lines = [line for line in r.stdout.splitlines() if line.startswith("{")]
     assert len(lines) == 1, r.stdout
@@ -49,3 +49,31 @@ def test_bench_json_line():
     cpu = d["cpu_baseline"]
     assert cpu["kind"] == "oracle" and cpu["value"] > 0 and cpu["cores"] >= 1
     assert cpu["unit"] == d["unit"] and cpu["sample"]
+
+
+def test_algorithmic_bytes_follow_the_element_size():
+    """Decode and prefill bytes per launch are counted at the workload's element size: the fp32 variant of
+    a workload moves exactly twice the bytes of its bf16 variant for the same FLOPs."""
+    sys.path.insert(0, ROOT)
+    import bench
+    from paper_2606_10537_amd import synth
+    from paper_2606_10537_amd._lib import PD_BF16, PD_FP32
+    w = synth.WORKLOADS[2]
+    wb = synth.Workload(**{**w.__dict__, "dtype": PD_BF16})
+    wf = synth.Workload(**{**w.__dict__, "dtype": PD_FP32})
+    pfb, pbb, dfb, dbb = bench.algorithmic(wb, 1)
+    pff, pbf, dff, dbf = bench.algorithmic(wf, 1)
+    assert (pff, dff) == (pfb, dfb)
+    assert pbf == 2 * pbb and dbf == 2 * dbb
+
+
+def test_cpu_baseline_full_tiny_workload():
+    """The oracle baseline of the tiny workload runs every unit of one job step on a process pool and
+    reports the host it ran on."""
+    sys.path.insert(0, ROOT)
+    import bench
+    from paper_2606_10537_amd import synth
+    r = bench.cpu_baseline(synth.WORKLOADS[1], 1.0, "auto")
+    assert r["mode"] == "full" and r["kind"] == "oracle" and r["value"] > 0
+    assert 1 <= r["cores"] <= bench.CPU_SHARE and r["affinity_cpus"] >= 1 and r["os_cpu_count"] >= 1
+    assert r["blas_threads_per_worker"] == 1 and r["numpy"] and r["sample"]
