@@ -39,18 +39,30 @@ def _run(cmd):
     return out
 
 
+# The checking build: kernels verify every kept chunk and slot index (see
+# pd_common.h); the library the path loads is the release build.
+LIB_CHECK = os.path.join(PKG, "libpd_check.so")
+
+
 def build(verbose: bool = False) -> str:
-    """Compile every source for gfx950 and link libpd.so; returns its path."""
-    os.makedirs(BUILD, exist_ok=True)
-    objs = [os.path.join(BUILD, s.replace(".hip", ".o")) for s in SOURCES]
-    cmds = [[HIPCC, *FLAGS, *EXTRA.get(s, []), "-c", os.path.join(CSRC, s), "-o", o] for s, o in zip(SOURCES, objs)]
-    with concurrent.futures.ThreadPoolExecutor(max_workers=min(4, len(cmds))) as ex:
+    """Compile every source for gfx950 and link libpd.so and the index-checking libpd_check.so; returns
+    the path of libpd.so."""
+    variants = [(LIB, BUILD, []), (LIB_CHECK, os.path.join(BUILD, "check"), ["-DPD_CHECK_INDICES=1"])]
+    cmds, links = [], []
+    for lib, objdir, defines in variants:
+        os.makedirs(objdir, exist_ok=True)
+        objs = [os.path.join(objdir, s.replace(".hip", ".o")) for s in SOURCES]
+        cmds += [[HIPCC, *FLAGS, *defines, *EXTRA.get(s, []), "-c", os.path.join(CSRC, s), "-o", o]
+                 for s, o in zip(SOURCES, objs)]
+        links.append((lib, objs))
+    with concurrent.futures.ThreadPoolExecutor(max_workers=8) as ex:
         for out in ex.map(_run, cmds):
             if verbose and out.strip():
                 print(out)
-    tmp = LIB + ".tmp"
-    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
-    os.replace(tmp, LIB)
+    for lib, objs in links:
+        tmp = lib + ".tmp"
+        _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
+        os.replace(tmp, lib)
     return LIB
 
 

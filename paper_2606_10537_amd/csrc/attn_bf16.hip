@@ -701,6 +701,9 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void decode_bf16_kernel(DecodeArgs 
   // shard within kDecodeTableRows rows), so tile loads need no index fetch.
   const int j_lo = t_begin * T::BN;
   const int j_hi = min(t_end * T::BN, n_sel);
+  __shared__ int bad_index;   // checking build: some kept row of this shard was out of range
+  if (kCheckIndices && tid == 0) bad_index = 0;
+  if (kCheckIndices) __syncthreads();
   if (p.compact) {
     for (int j = j_lo + tid; j < j_hi; j += T::NT) rowtab[j - j_lo] = j;
   } else {
@@ -708,8 +711,14 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void decode_bf16_kernel(DecodeArgs 
     const int32_t* tslot = p.tok_slot + (size_t)b * p.K * p.Bt;
     for (int j = j_lo + tid; j < j_hi; j += T::NT) {
       const int kk = j / (1 + p.Bt), s = j - kk * (1 + p.Bt);
-      const int slot = s == 0 ? 0 : tslot[kk * p.Bt + s - 1];
-      rowtab[j - j_lo] = cidx[kk] * p.Hkv * C1 + slot;
+      int slot = s == 0 ? 0 : tslot[kk * p.Bt + s - 1];
+      int chunk = cidx[kk];
+      if (kCheckIndices && !kept_row_ok(chunk, slot, s == 0, p.N, p.C)) {
+        chunk = 0;
+        slot = 0;
+        bad_index = 1;
+      }
+      rowtab[j - j_lo] = chunk * p.Hkv * C1 + slot;
     }
   }
   __syncthreads();
@@ -804,8 +813,9 @@ __global__ __launch_bounds__(Tile<D>::NT, 1) void decode_bf16_kernel(DecodeArgs 
     const int hq = g * p.G + rho / p.Ld;
     const int rr = rho % p.Ld;
     const float ltot = st[j].l + __shfl_xor(st[j].l, 32);
-    const float inv = 1.0f / ltot;
-    const float lse2 = st[j].m + __log2f(ltot);
+    float inv = 1.0f / ltot;
+    float lse2 = st[j].m + __log2f(ltot);
+    if (kCheckIndices && bad_index) inv = lse2 = __uint_as_float(kNanWord);
     if (p.S == 1) {
       const size_t orow = (((size_t)b * p.Ld + rr) * p.Hq + hq) * D;
       if (p.out_f32) store_row_f32<D>(reinterpret_cast<float*>(p.o_dec) + orow, st[j], inv, grp);

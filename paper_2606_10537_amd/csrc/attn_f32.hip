@@ -241,6 +241,9 @@ __global__ __launch_bounds__(64) void decode_f32_kernel(DecodeArgs p) {
   const int32_t* cidx = p.chunk_idx + (size_t)b * p.K;
   const int32_t* tslot = p.tok_slot + (size_t)b * p.K * p.Bt;
   constexpr int CPR = D / 4;
+  __shared__ int bad_index;   // checking build: some kept row of this shard was out of range
+  if (kCheckIndices && tid == 0) bad_index = 0;
+  if (kCheckIndices) __syncthreads();
   for (int t = t_begin; t < t_end; ++t) {
     for (int i = tid; i < kF32Keys * CPR; i += kF32Rows) {
       const int kk = i / CPR, c = i % CPR;
@@ -252,8 +255,14 @@ __global__ __launch_bounds__(64) void decode_f32_kernel(DecodeArgs p) {
         vv = ld4(v_cache + off);
       } else if (j < n_sel) {
         const int q = j / (1 + p.Bt), s = j - q * (1 + p.Bt);
-        const int slot = s == 0 ? 0 : tslot[q * p.Bt + s - 1];
-        const size_t off = (cache_bg + (size_t)cidx[q] * p.Hkv * C1 + slot) * D + 4 * c;
+        int slot = s == 0 ? 0 : tslot[q * p.Bt + s - 1];
+        int chunk = cidx[q];
+        if (kCheckIndices && !kept_row_ok(chunk, slot, s == 0, p.N, p.C)) {
+          chunk = 0;
+          slot = 0;
+          bad_index = 1;
+        }
+        const size_t off = (cache_bg + (size_t)chunk * p.Hkv * C1 + slot) * D + 4 * c;
         kv = ld4(k_cache + off);
         vv = ld4(v_cache + off);
       } else if (j < n_sel + p.n_static) {
@@ -273,8 +282,9 @@ __global__ __launch_bounds__(64) void decode_f32_kernel(DecodeArgs p) {
     __syncthreads();
   }
   if (r >= p.Ld) return;
-  const float inv = 1.0f / st.l;
-  const float lse2 = st.m + __log2f(st.l);
+  float inv = 1.0f / st.l;
+  float lse2 = st.m + __log2f(st.l);
+  if (kCheckIndices && bad_index) inv = lse2 = __uint_as_float(kNanWord);
   if (p.S == 1) {
     row_store<D>(reinterpret_cast<float*>(p.o_dec) + (((size_t)b * p.Ld + r) * p.Hq + h) * D, st, inv);
     if (p.lse_dec) p.lse_dec[((size_t)b * p.Hq + h) * p.Ld + r] = lse2 * kLn2;

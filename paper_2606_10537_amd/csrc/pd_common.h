@@ -49,6 +49,21 @@ __device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Index checks of the checking build (compiled with PD_CHECK_INDICES): a kept
+// chunk outside 0..N-1 or a kept slot outside 1..C (slot 0, the BOS row, is
+// implied) is replaced by slot 0 of chunk 0 before anything is read, and every
+// output that depended on it is written as NaN.  Release builds trust the
+// indices, which the selection kernels produce in range.
+#ifdef PD_CHECK_INDICES
+constexpr bool kCheckIndices = true;
+#else
+constexpr bool kCheckIndices = false;
+#endif
+constexpr uint32_t kNanWord = 0x7FC07FC0u;   // a NaN as fp32 and as two bf16
+__device__ __forceinline__ bool kept_row_ok(int chunk, int slot, bool bos, int N, int C) {
+  return chunk >= 0 && chunk < N && (bos ? slot == 0 : (slot >= 1 && slot <= C));
+}
+
 // Monotone map of an fp32 value to uint32 (ascending order preserved; -0 == +0).
 __device__ __forceinline__ uint32_t float_order_key(float f) {
   if (f == 0.0f) f = 0.0f;

@@ -490,10 +490,14 @@ __global__ __launch_bounds__(256) void gather_selected_kernel(const u32x4* k_cac
   const int g = (int)(r % Hkv);
   const int b = (int)(r / Hkv);
   const int kk = j / (1 + Bt), sl = j - kk * (1 + Bt);
-  const int slot = sl == 0 ? 0 : tok_slot[((size_t)b * K + kk) * Bt + sl - 1];
-  const size_t src = ((((size_t)b * N + chunk_idx[(size_t)b * K + kk]) * Hkv + g) * C1 + slot) * cpr + c;
-  k_sel[gid] = k_cache[src];
-  v_sel[gid] = v_cache[src];
+  int slot = sl == 0 ? 0 : tok_slot[((size_t)b * K + kk) * Bt + sl - 1];
+  int chunk = chunk_idx[(size_t)b * K + kk];
+  const bool bad = kCheckIndices && !kept_row_ok(chunk, slot, sl == 0, N, C1 - 1);
+  if (bad) chunk = slot = 0;
+  const size_t src = ((((size_t)b * N + chunk) * Hkv + g) * C1 + slot) * cpr + c;
+  const u32x4 nan4 = {kNanWord, kNanWord, kNanWord, kNanWord};
+  k_sel[gid] = bad ? nan4 : k_cache[src];
+  v_sel[gid] = bad ? nan4 : v_cache[src];
 }
 
 hipError_t launch_gather_selected(const void* k_cache, const void* v_cache, const int32_t* chunk_idx,
@@ -527,11 +531,15 @@ __global__ __launch_bounds__(256) void gather_joint_kernel(JointArgs a) {
   const bool kept = j < n_sel;
   int kk = a.K - 1, slot = 0;
   size_t n = 0, qm_row = 0;
+  bool bad = false;
   if (kept) {
     kk = j / (1 + a.Bt);
     const int sl = j - kk * (1 + a.Bt);
     slot = sl == 0 ? 0 : a.tok_slot[((size_t)b * a.K + kk) * a.Bt + sl - 1];
-    n = (size_t)b * a.N + a.chunk_idx[(size_t)b * a.K + kk];
+    int chunk = a.chunk_idx[(size_t)b * a.K + kk];
+    bad = kCheckIndices && !kept_row_ok(chunk, slot, sl == 0, a.N, a.C);
+    if (bad) chunk = slot = 0;
+    n = (size_t)b * a.N + chunk;
   } else {
     qm_row = (a.qm_per_chunk ? (size_t)b * a.N : (size_t)b) * (size_t)(a.Lq + a.Lm) + (j - n_sel);
   }
@@ -598,6 +606,7 @@ __global__ __launch_bounds__(256) void gather_joint_kernel(JointArgs a) {
         }
       }
     }
+    if (bad) lo = hi = u32x4{kNanWord, kNanWord, kNanWord, kNanWord};
     d4[cp] = lo;
     d4[cp + CP] = hi;
     void* pref = tensor == 1 ? a.k_pref : (tensor == 2 ? a.v_pref : nullptr);
