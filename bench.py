@@ -642,7 +642,7 @@ def workload_summary(w, m):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (got --gpus {args.gpus}); the path shards by "
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the path shards by "
               "sequence with no communication, so multi-GPU figures are not produced.", file=sys.stderr)
         sys.exit(2)
     from paper_2606_10537_amd import synth
