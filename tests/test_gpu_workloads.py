@@ -7,9 +7,10 @@ chunk selection of every sequence at several steps (rule A), the token sets of
 the kept chunks of one sequence (rule A against the oracle's Eq. 5 scores), and
 decode outputs of listed (sequence, head) pairs with the oracle run on the
 GPU's own indices.  The 32K workloads also get the full-size sample: prefill of
-two sequences x every chunk x every head, selections at steps 0, T/2 and T-1
-(for the 32-layer workload: of every layer), decode of two sequences x every
-head at T/2.
+two sequences x every chunk x every head (for the 32-layer workload on its
+first and last layer), and at steps 0, T/2 and T-1 the selections of every
+sequence and the decode of two sequences x every head; the 32-layer workload
+also has the selections of every layer checked.
 """
 
 import numpy as np
@@ -105,72 +106,79 @@ def test_workload4_32k_b4_bf16_out():
                  out_fp32=0)
 
 
-def full_size_sample(wid, seqs=(0, 1)):
-    """The full-size sample of one layer, with fp32 outputs (the strict 1e-2 bar): prefill O of the
-    sequences `seqs` x every chunk x every head (oracle on a process pool), with their cache bits, key
-    means, Eq. 5 scores and token ranks; the key means of every chunk; at steps 0, T/2 and T-1 the
-    selection of every sequence (rule A against the oracle's scores from the oracle's key means) and its
-    token sets; at T/2 the decode O of `seqs` x every head, the oracle run on the GPU's indices.  Returns
-    the count of selections inside rule A's band."""
+def full_size_sample(wid, seqs=(0, 1), layers=(0,)):
+    """The full-size sample, one layer of `layers` resident at a time, with fp32 outputs (the strict 1e-2
+    bar): prefill O of the sequences `seqs` x every chunk x every head (oracle on a process pool), with
+    their cache bits, key means, Eq. 5 scores and token ranks; the key means of every chunk; at steps 0,
+    T/2 and T-1 the selection of every sequence (rule A against the oracle's scores from the oracle's key
+    means) and its token sets, and the decode O of `seqs` x every head, the oracle run on the GPU's
+    indices.  Returns the count of selections inside rule A's band."""
     from oracle_pool import OraclePool
     w = synth.WORKLOADS[wid]
     d = w.dims()
     d.out_fp32 = 1
     B, N, Hq = d.batch, d.n_chunks, d.n_heads_q
-    print(f"[workload {wid} sample] prefill of layer 0 at B={B}", flush=True)
-    x = synth.make_prefill(w, 0, "cuda")
-    out = run_prefill(d, x)
-    torch.cuda.synchronize()
     sl = list(seqs)
-    host = {k: v[sl].float().cpu().numpy() for k, v in x.items()}
-    host["o"] = out["o"][sl].float().cpu().numpy()
-    units = [(i, n, h) for i in range(len(sl)) for n in range(N) for h in range(Hq)]
-    print(f"[workload {wid} sample] {len(units)} oracle prefill units", flush=True)
-    with OraclePool(host) as pool:
-        res = pool.prefill_units(units, d.q_len, 1e-2, 0.0)
-    worst = max(r[3] for r in res)
-    assert worst <= 0, f"prefill O exceeds the 1e-2 bar by {worst:.3g} (worst unit {max(res, key=lambda r: r[3])[:3]})"
-    e = np.zeros((len(sl), N, d.chunk_len))
-    for i, n, h, _, eh in res:
-        e[i, n] += eh
-    for i, b in enumerate(sl):
-        np.testing.assert_allclose(h64(out["tok_score"][b]), e[i], rtol=0, atol=1e-4)
-        for n in range(N):
-            check_rank_consistent(e[i, n], out["tok_rank"][b, n].cpu().numpy())
-            for name in ("k", "v"):
-                want = oracle.cache_ref(bits(x[f"{name}_pre"][b:b + 1, n:n + 1]))[0, 0]
-                assert np.array_equal(bits(out[f"{name}_cache"][b, n]), want), (name, b, n)
-    km_ref = np.zeros((B, N, d.n_heads_kv, d.head_dim))
-    for b in range(B):
-        for n in range(N):
-            km_ref[b, n] = oracle.key_mean_ref(h64(x["k_pre"][b:b + 1, n:n + 1]))[0, 0]
-    np.testing.assert_allclose(h64(out["key_mean"]), km_ref, rtol=1e-5, atol=1e-6 * np.abs(km_ref).max())
     unpinned = total = 0
     T = w.steps
-    for t in (0, T // 2, T - 1):
-        dec = synth.make_decode(w, 0, t, "cuda")
-        ci, tsl, cs = run_select(d, w.top_k, w.tok_budget, dec["q_dec"], out["key_mean"], out["tok_rank"])
+    for layer in layers:
+        print(f"[workload {wid} sample] prefill of layer {layer} at B={B}", flush=True)
+        x = synth.make_prefill(w, layer, "cuda")
+        out = run_prefill(d, x)
         torch.cuda.synchronize()
-        s_ref = oracle.chunk_scores_ref(h64(dec["q_dec"]), km_ref)
-        np.testing.assert_allclose(h64(cs), s_ref, rtol=1e-4, atol=1e-4)
-        cih = ci.cpu().numpy()
-        for b in range(B):
-            unpinned += check_topk_rule_a(s_ref[b], cih[b], w.top_k)
-            total += N
-        assert np.array_equal(tsl.cpu().numpy(),
-                              oracle.tokens_by_rank_ref(out["tok_rank"].cpu().numpy(), cih, w.tok_budget))
+        host = {k: v[sl].float().cpu().numpy() for k, v in x.items()}
+        host["o"] = out["o"][sl].float().cpu().numpy()
+        units = [(i, n, h) for i in range(len(sl)) for n in range(N) for h in range(Hq)]
+        print(f"[workload {wid} sample] {len(units)} oracle prefill units", flush=True)
+        with OraclePool(host) as pool:
+            res = pool.prefill_units(units, d.q_len, 1e-2, 0.0)
+        del host
+        worst = max(r[3] for r in res)
+        assert worst <= 0, (f"prefill O exceeds the 1e-2 bar by {worst:.3g} (layer {layer}, worst unit "
+                            f"{max(res, key=lambda r: r[3])[:3]})")
+        e = np.zeros((len(sl), N, d.chunk_len))
+        for i, n, h, _, eh in res:
+            e[i, n] += eh
         for i, b in enumerate(sl):
-            for kk, n in enumerate(cih[b].tolist()):
-                unpinned += check_topk_rule_a(e[i, n], tsl[b, kk].cpu().numpy() - 1, w.tok_budget)
-                total += d.chunk_len
-        if t == T // 2:
+            np.testing.assert_allclose(h64(out["tok_score"][b]), e[i], rtol=0, atol=1e-4)
+            for n in range(N):
+                check_rank_consistent(e[i, n], out["tok_rank"][b, n].cpu().numpy())
+                for name in ("k", "v"):
+                    want = oracle.cache_ref(bits(x[f"{name}_pre"][b:b + 1, n:n + 1]))[0, 0]
+                    assert np.array_equal(bits(out[f"{name}_cache"][b, n]), want), (layer, name, b, n)
+        km_ref = np.zeros((B, N, d.n_heads_kv, d.head_dim))
+        for b in range(B):
+            for n in range(N):
+                km_ref[b, n] = oracle.key_mean_ref(h64(x["k_pre"][b:b + 1, n:n + 1]))[0, 0]
+        np.testing.assert_allclose(h64(out["key_mean"]), km_ref, rtol=1e-5, atol=1e-6 * np.abs(km_ref).max())
+        del out["o"]
+        torch.cuda.empty_cache()
+        for t in (0, T // 2, T - 1):
+            dec = synth.make_decode(w, layer, t, "cuda")
+            ci, tsl, cs = run_select(d, w.top_k, w.tok_budget, dec["q_dec"], out["key_mean"], out["tok_rank"])
+            torch.cuda.synchronize()
+            s_ref = oracle.chunk_scores_ref(h64(dec["q_dec"]), km_ref)
+            np.testing.assert_allclose(h64(cs), s_ref, rtol=1e-4, atol=1e-4)
+            cih = ci.cpu().numpy()
+            for b in range(B):
+                unpinned += check_topk_rule_a(s_ref[b], cih[b], w.top_k)
+                total += N
+            assert np.array_equal(tsl.cpu().numpy(),
+                                  oracle.tokens_by_rank_ref(out["tok_rank"].cpu().numpy(), cih, w.tok_budget))
+            for i, b in enumerate(sl):
+                for kk, n in enumerate(cih[b].tolist()):
+                    unpinned += check_topk_rule_a(e[i, n], tsl[b, kk].cpu().numpy() - 1, w.tok_budget)
+                    total += d.chunk_len
             o, lse = run_decode(d, w.top_k, w.tok_budget, dec, out, ci, tsl, x["k_qm"], x["v_qm"], w.q_len)
             torch.cuda.synchronize()
             decode_check(d, w.top_k, w.tok_budget, dec, out, ci, tsl, x["k_qm"], x["v_qm"], w.q_len, o, lse,
                          batches=sl)
-        print(f"[workload {wid} sample] step {t} ok", flush=True)
-    print(f"[rule A] workload {wid}, layer 0: {unpinned} of {total} candidates unpinned (inside the 1e-3 band)",
-          flush=True)
+            del o, lse, dec
+            print(f"[workload {wid} sample] layer {layer} step {t} ok", flush=True)
+        del x, out
+        torch.cuda.empty_cache()
+    print(f"[rule A] workload {wid}, layers {tuple(layers)}: {unpinned} of {total} candidates unpinned (inside "
+          f"the 1e-3 band)", flush=True)
     return unpinned
 
 
@@ -179,7 +187,7 @@ def test_workload4_32k_b4_sample():
 
 
 def test_workload5_32k_layer_b8_sample():
-    full_size_sample(5, seqs=(0, 7))
+    full_size_sample(5, seqs=(0, 7), layers=(0, 31))
 
 
 def selection_all_layers(wid):
