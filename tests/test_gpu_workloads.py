@@ -6,7 +6,10 @@ their real sizes; the oracle checks sampled units: prefill O / cache / key means
 chunk selection of every sequence at several steps (rule A), the token sets of
 the kept chunks of one sequence (rule A against the oracle's Eq. 5 scores), and
 decode outputs of listed (sequence, head) pairs with the oracle run on the
-GPU's own indices.  The 32K workloads also get the full-size sample: prefill of
+GPU's own indices.  The 8K and 16K workloads (one sequence each) are also
+checked in full: every chunk and head of the prefill, and at steps 0, T/2 and
+T-1 the selection and every head of the decode.  The 32K workloads also get
+the full-size sample: prefill of
 two sequences x every chunk x every head (for the 32-layer workload on its
 first and last layer), and at steps 0, T/2 and T-1 the selections of every
 sequence and the decode of two sequences x every head; the 32-layer workload
@@ -180,6 +183,16 @@ def full_size_sample(wid, seqs=(0, 1), layers=(0,)):
     print(f"[rule A] workload {wid}, layers {tuple(layers)}: {unpinned} of {total} candidates unpinned (inside "
           f"the 1e-3 band)", flush=True)
     return unpinned
+
+
+def test_workload2_8k_full():
+    """The 8K workload's one sequence in full: every chunk and head of the prefill, selection and every
+    head of the decode at steps 0, T/2 and T-1."""
+    full_size_sample(2, seqs=(0,))
+
+
+def test_workload3_16k_gqa_full():
+    full_size_sample(3, seqs=(0,))
 
 
 def test_workload4_32k_b4_sample():
