@@ -120,9 +120,26 @@ int decode_qtiles(const pd_dims* d) {
   const int G = d->n_heads_q / d->n_heads_kv;
   return d->dtype == PD_BF16 ? cdiv((long long)G * d->dec_len, pd::kBf16Rows) : cdiv(d->dec_len, 64);
 }
-int decode_units(const pd_dims* d) {
-  return d->dtype == PD_BF16 ? d->batch * d->n_heads_kv * decode_qtiles(d)
-                             : d->batch * d->n_heads_q * decode_qtiles(d);
+long long decode_units(const pd_dims* d) {
+  return (long long)d->batch * (d->dtype == PD_BF16 ? d->n_heads_kv : d->n_heads_q) * decode_qtiles(d);
+}
+
+// Launch sizes that must fit one grid dimension: the decode (work items x
+// shards), its Split-S merge (one thread per 4 output elements), and the
+// chunk-score pass over `rows` query rows (sequence x head x 128-row split).
+pd_status check_decode_grid(const pd_dims* d, int S) {
+  const long long total = decode_units(d) * S;
+  const long long merge = ((long long)d->batch * d->n_heads_q * d->dec_len * (d->head_dim / 4) + 255) / 256;
+  if (total >= (1LL << 31) || (S > 1 && merge >= (1LL << 31)))
+    return fail(PD_ERR_BAD_DIMS, "decode of batch=%d, dec_len=%d with %d shards is too large for one launch",
+                d->batch, d->dec_len, S);
+  return PD_OK;
+}
+pd_status check_select_grid(const pd_dims* d, int rows) {
+  if ((long long)d->batch * d->n_heads_q * pd::select_row_splits(rows) >= (1LL << 31))
+    return fail(PD_ERR_BAD_DIMS, "chunk scoring of batch=%d over %d query rows is too large for one launch",
+                d->batch, rows);
+  return PD_OK;
 }
 
 // Shard counts for a decode call whose KV has n_sel prefix rows per (sequence,
@@ -142,7 +159,7 @@ int requested_splits(const pd_dims* d, long long n_sel, int num_splits) {
   if (s <= 0) {
     const long long lkv0 = n_sel + d->dec_len;
     const int max_by_len = std::max(1, cdiv(lkv0, 64) / 4);
-    const int want = cdiv(kTargetWorkgroups, std::max(1, decode_units(d)));
+    const int want = cdiv(kTargetWorkgroups, std::max(1LL, decode_units(d)));
     s = std::max(1, std::min(std::min(want, max_by_len), kMaxSplits));
   }
   return std::max(s, min_splits(d, n_sel));
@@ -238,11 +255,16 @@ size_t pd_workspace_bytes(const pd_dims* d, int32_t top_k, int32_t tok_budget, i
   if (check_dims(d) != PD_OK) return 0;
   switch (which) {
     case 0: return prefill_ws(d).total;
-    case 1: return select_ws(d);
-    case 2:
+    case 1:
+      if (check_select_grid(d, std::max(d->dec_len, std::max(d->m_len, 1))) != PD_OK) return 0;
+      return select_ws(d);
+    case 2: {
       if (top_k < 1 || tok_budget < 1 || num_splits < 0 || num_splits > kMaxSplits) return 0;
       if (check_decode_rows(d, n_sel_of(top_k, tok_budget), 0) != PD_OK) return 0;
-      return decode_ws_bytes(d, requested_splits(d, n_sel_of(top_k, tok_budget), num_splits));
+      const int S = requested_splits(d, n_sel_of(top_k, tok_budget), num_splits);
+      if (check_decode_grid(d, S) != PD_OK) return 0;
+      return decode_ws_bytes(d, S);
+    }
     default: return 0;
   }
 }
@@ -447,7 +469,7 @@ pd_status select_args(const pd_dims* d, int32_t top_k, int32_t tok_budget, const
   a->NS = pd::select_row_splits(a->q_rows);
   a->bf16 = d->dtype == PD_BF16;
   a->scale = scale_of(d);
-  return PD_OK;
+  return check_select_grid(d, a->q_rows);
 }
 
 void place_select_ws(void* ws, pd::SelectArgs* a) { a->partial = (float*)ws; }
@@ -500,6 +522,7 @@ pd_status pd_score_select_static(const pd_dims* d, int32_t top_k, int32_t tok_bu
   a.q_row0 = d->q_len;
   a.q_bstride = (d->qm_per_chunk ? d->n_chunks : 1) * (d->q_len + d->m_len);
   a.NS = pd::select_row_splits(a.q_rows);
+  PD_RETURN_IF(check_select_grid(d, a.q_rows));
   return hip_status(pd::launch_score_select(a, (hipStream_t)stream), "static score/select kernels");
 }
 
@@ -611,6 +634,7 @@ static pd_status decode_core(const pd_dims* d, int top_k, int tok_budget, long l
   PD_RETURN_IF(check_decode_rows(d, n_sel, n_static));
   const int S_req = requested_splits(d, n_sel, num_splits);
   const int S = effective_splits(d, n_sel, n_static, num_splits);
+  PD_RETURN_IF(check_decode_grid(d, S_req));
   PD_RETURN_IF(check_ws(workspace, ws_bytes, decode_ws_bytes(d, S_req)));
 
   const bool bf16 = d->dtype == PD_BF16;
@@ -644,7 +668,7 @@ static pd_status decode_core(const pd_dims* d, int top_k, int tok_budget, long l
   a.out_f32 = d->out_fp32;
   a.scale_log2 = scale_of(d) * 1.4426950408889634f;
   a.n_qt = decode_qtiles(d);
-  a.total = decode_units(d) * S;
+  a.total = (int)(decode_units(d) * S);
   if (S > 1) {
     const size_t rows = (size_t)S * a.B * a.Hq * a.Ld;
     a.o_part = (float*)workspace;
@@ -699,7 +723,9 @@ size_t pd_compact_workspace_bytes(const pd_dims* d, int32_t n_sel, int32_t num_s
   if (check_dims(d) != PD_OK || n_sel < 0 || n_sel > kMaxCompactRows || num_splits < 0 || num_splits > kMaxSplits)
     return 0;
   if (check_decode_rows(d, n_sel, 0) != PD_OK) return 0;
-  return decode_ws_bytes(d, requested_splits(d, n_sel, num_splits));
+  const int S = requested_splits(d, n_sel, num_splits);
+  if (check_decode_grid(d, S) != PD_OK) return 0;
+  return decode_ws_bytes(d, S);
 }
 
 }  // extern "C"

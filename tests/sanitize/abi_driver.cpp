@@ -93,6 +93,13 @@ int main() {
   EXPECT(pd_gather_joint(&d, 2, 64, Ai, Ai, A, A, A, A, A, A, -1.0, A, A, A, nullptr, nullptr, nullptr), PD_ERR_BAD_DIMS);
   EXPECT(pd_gather_joint(&d, 2, 64, Ai, Ai, A, A, A, A, A, A, 1e4, A, A, A, A, nullptr, nullptr), PD_ERR_NULL_PTR);
   EXPECT(pd_mfma_rate_probe(0, 10, Af, nullptr), PD_ERR_BAD_DIMS);
+  // launch grids past one dimension: decode work items and chunk-score splits
+  pd_dims tall = dims();
+  tall.batch = 1 << 20; tall.n_chunks = 1; tall.chunk_len = 1; tall.q_len = 1; tall.m_len = 0;
+  tall.dec_len = 1 << 19; tall.n_heads_q = 1; tall.n_heads_kv = 1; tall.head_dim = 128;
+  EXPECT(pd_score_select(&tall, 1, 1, A, Af, Ai, Ai, Ai, nullptr, A, big, nullptr), PD_ERR_BAD_DIMS);
+  EXPECT(pd_sparse_decode_attn(&tall, 1, 1, A, A, A, A, A, Ai, Ai, A, A, 1, A, nullptr, 0, A, big, nullptr), PD_ERR_BAD_DIMS);
+  if (pd_workspace_bytes(&tall, 1, 1, 0, 2) != 0) { std::printf("FAIL: size query accepted a huge decode\n"); ++failures; }
 
   // queries and strings
   if (pd_cache_bytes(&d) != size_t(1) * 4 * 4 * 129 * 64 * 2) { std::printf("FAIL: pd_cache_bytes\n"); ++failures; }

@@ -189,6 +189,28 @@ def test_decode_row_offsets_bounded(lib):
                                      0, A, 1 << 40, None) == 2
 
 
+def test_launch_grids_bounded(lib):
+    """A call whose decode grid (work items x shards) or chunk-score grid (sequences x heads x 128-row
+    splits) would not fit one launch dimension is rejected on the host, and the size queries return 0;
+    nothing is launched."""
+    d = dims(batch=1 << 20, n_chunks=1, chunk_len=1, q_len=1, m_len=0, dec_len=1 << 19, n_heads_q=1,
+             n_heads_kv=1, head_dim=128)
+    c = ctypes.byref(d.c())
+    assert (1 << 20) * ((1 << 19) // 256) >= 1 << 31           # decode work items
+    assert lib.pd_score_select(c, 1, 1, A, A, A, A, A, None, A, 1 << 40, None) == 2
+    assert b"too large" in lib.pd_last_error_message()
+    assert lib.pd_score_select_noalloc(c, 1, 1, A, A, A, A, A, None, None) == 2
+    assert _lib.pd_workspace_bytes(d, 0, 0, 0, 1) == 0
+    assert lib.pd_sparse_decode_attn(c, 1, 1, A, A, A, A, A, A, A, A, A, 1, A, None, 0, A, 1 << 40, None) == 2
+    assert b"too large" in lib.pd_last_error_message()
+    assert _lib.pd_workspace_bytes(d, 1, 1, 0, 2) == 0
+    assert _lib.pd_compact_workspace_bytes(d, 2, 0) == 0
+    # the same sizes at batch 1 are accepted by the size queries
+    d1 = dims(batch=1, n_chunks=1, chunk_len=1, q_len=1, m_len=0, dec_len=1 << 19, n_heads_q=1, n_heads_kv=1,
+              head_dim=128)
+    assert _lib.pd_workspace_bytes(d1, 0, 0, 0, 1) > 0
+
+
 def test_select_ranked_validation(lib):
     c = ctypes.byref(dims().c())
     call = lambda k=2, bt=64, cs=A, low=1, tr=A, ci=A, dd=c: lib.pd_select_ranked(dd, k, bt, cs, low, tr, ci, A, None)
