@@ -19,6 +19,11 @@
  *   a thread-local message is kept for pd_last_error_message().  A failed
  *   launch returns PD_ERR_HIP.  Faults inside a kernel surface at the caller's
  *   next synchronisation on `stream`.
+ * - Size limits besides those of each entry point: element offsets inside one
+ *   sequence's cache, chunk sequence, decode block or decode KV rows stay
+ *   below 2^31, and every launch grid (prefill, selection, decode, Split-S
+ *   merge) below 2^31 workgroups; larger calls return PD_ERR_BAD_DIMS, and
+ *   the size queries return 0 for them.
  * - Element type: all Q/K/V/O/cache tensors of one call have the type
  *   `dims->dtype` (bf16 or fp32).  Scores, key means and LSEs are fp32;
  *   indices are int32.  Arithmetic is fp32 (bf16 inputs feed bf16 matrix
