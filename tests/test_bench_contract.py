@@ -67,6 +67,27 @@ def test_algorithmic_bytes_follow_the_element_size():
     assert pbf == 2 * pbb and dbf == 2 * dbb
 
 
+def test_algorithmic_work_of_the_32k_workloads():
+    """The work the roofline fractions are taken against, pinned to the figures derived by hand from the
+    method's shapes (4 S_c^2 d FLOP per prefill (chunk, head); 4 L_d L_kv d per decode (sequence, head);
+    decode bytes: K and V of the L_kv rows per KV head plus Q read and O written per query head)."""
+    sys.path.insert(0, ROOT)
+    import bench
+    from paper_2606_10537_amd import synth
+    # 32K, one layer, batch 8: S_c = 1 + 1024 + 128 + 512 = 1665, L_kv = 4 * 257 + 128 + 512 = 1668
+    pf, pb, df, db = bench.algorithmic(synth.WORKLOADS[5], 1)
+    assert pf == 4 * 1665 ** 2 * 128 * 8 * 32 * 32              # 11.63 TFLOP per layer
+    assert abs(pf / (8 * 32 * 32) - 1.419e9) < 1e6              # 1.419 GFLOP per (chunk, head)
+    assert df == 4 * 512 * 1668 * 128 * 8 * 32                  # 111.9 GFLOP per launch
+    assert abs(df / (8 * 32) - 437.3e6) < 1e5                   # 437.3 MFLOP per (sequence, head)
+    assert db == 2 * 128 * 8 * (2 * 1668 * 32 + 2 * 512 * 32)   # 285.7 MB per launch
+    assert abs(db / (8 * 32) - 1.116e6) < 1e3                   # 1.116 MB per (sequence, head)
+    assert 391 < df / db < 393                                  # arithmetic intensity, FLOP per byte
+    # 32K batch 4 is the same per (sequence, head)
+    pf4, _, df4, db4 = bench.algorithmic(synth.WORKLOADS[4], 1)
+    assert (pf4, df4, db4) == (pf / 2, df / 2, db / 2)
+
+
 def test_cpu_baseline_full_tiny_workload():
     """The oracle baseline of the tiny workload runs every unit of one job step on a process pool and
     reports the host it ran on."""
